@@ -1,0 +1,334 @@
+// C ABI of the eviction library: argument validation, workspace layout and
+// stream-ordered launch sequencing.  No device memory is allocated here and
+// the stream is never synchronised.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/nacl.h"
+#include "internal.h"
+
+namespace {
+
+thread_local char g_detail[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_detail, sizeof(g_detail), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(NACL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
+
+struct Layout {
+  size_t pos, lse, part, keys, total;
+  int n_chunks_max;
+};
+
+Layout layout_of(const nacl_problem* p) {
+  Layout l;
+  const size_t BH = (size_t)p->B * p->H;
+  l.n_chunks_max = (p->L + nacl::kScoreChunkKeys - 1) / nacl::kScoreChunkKeys;
+  size_t off = 0;
+  l.pos = off;
+  off += align_up((size_t)p->P * sizeof(int32_t));
+  l.lse = off;
+  off += align_up(BH * p->P * sizeof(float));
+  l.part = off;
+  off += align_up(BH * l.n_chunks_max * p->P * sizeof(float2));
+  l.keys = off;
+  off += align_up(BH * p->L * sizeof(uint32_t));
+  l.total = off;
+  return l;
+}
+
+// Byte extent [lo, hi) of a strided [B, H, L, D] tensor.
+void extent(const void* base, const int64_t st[3], const nacl_problem* p, uintptr_t& lo,
+            uintptr_t& hi) {
+  const int64_t last = (int64_t)(p->B - 1) * st[0] + (int64_t)(p->H - 1) * st[1] +
+                       (int64_t)(p->L - 1) * st[2] + p->D;
+  lo = (uintptr_t)base;
+  hi = lo + (uintptr_t)last * elt_bytes(p->dtype);
+}
+
+bool overlaps(uintptr_t a0, uintptr_t a1, uintptr_t b0, uintptr_t b1) { return a0 < b1 && b0 < a1; }
+
+int check_problem(const nacl_problem* p) {
+  if (!p) return fail(NACL_ERR_INVALID_ARG, "problem is NULL");
+  if (p->B < 1 || p->H < 1 || p->L < 1)
+    return fail(NACL_ERR_INVALID_ARG, "B, H, L must be >= 1 (got %d, %d, %d)", p->B, p->H, p->L);
+  if (p->L > NACL_MAX_L) return fail(NACL_ERR_UNSUPPORTED, "L = %d exceeds %d", p->L, NACL_MAX_L);
+  if ((int64_t)p->B * p->H > 65535)
+    return fail(NACL_ERR_UNSUPPORTED, "B * H = %lld exceeds 65535", (long long)p->B * p->H);
+  if (p->D != 64 && p->D != 128) return fail(NACL_ERR_UNSUPPORTED, "D must be 64 or 128 (got %d)", p->D);
+  if (p->dtype != NACL_F32 && p->dtype != NACL_BF16)
+    return fail(NACL_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
+  if (p->P < 1 || p->P > p->L) return fail(NACL_ERR_INVALID_ARG, "P must lie in [1, L] (got %d)", p->P);
+  if (p->P > NACL_MAX_P) return fail(NACL_ERR_UNSUPPORTED, "P = %d exceeds %d", p->P, NACL_MAX_P);
+  if (p->n_protect < 0 || p->n_protect > p->P)
+    return fail(NACL_ERR_INVALID_ARG, "n_protect must lie in [0, P] (got %d)", p->n_protect);
+  if (!(std::isfinite(p->sm_scale) && p->sm_scale > 0.f))
+    return fail(NACL_ERR_INVALID_ARG, "sm_scale must be finite and > 0");
+  if (!p->proxy_pos) return fail(NACL_ERR_INVALID_ARG, "proxy_pos is NULL");
+  for (int i = 0; i < p->P; ++i) {
+    const int32_t x = p->proxy_pos[i];
+    if (x < 0 || x >= p->L)
+      return fail(NACL_ERR_INVALID_ARG, "proxy_pos[%d] = %d outside [0, L)", i, x);
+    if (i && x <= p->proxy_pos[i - 1])
+      return fail(NACL_ERR_INVALID_ARG, "proxy_pos must be strictly increasing (index %d)", i);
+  }
+  const int eb = elt_bytes(p->dtype);
+  const int64_t* strides[3] = {p->q_stride, p->k_stride, p->v_stride};
+  const char* names[3] = {"q_stride", "k_stride", "v_stride"};
+  for (int t = 0; t < 3; ++t)
+    for (int i = 0; i < 3; ++i) {
+      if (strides[t][i] < 0) return fail(NACL_ERR_INVALID_ARG, "%s[%d] < 0", names[t], i);
+      if ((strides[t][i] * eb) % 16)
+        return fail(NACL_ERR_INVALID_ARG, "%s[%d] * element size must be a multiple of 16 bytes",
+                    names[t], i);
+    }
+  return NACL_OK;
+}
+
+bool aligned16(const void* ptr) { return ((uintptr_t)ptr & 15u) == 0; }
+
+int check_ws(const nacl_problem* p, const void* ws, size_t ws_bytes) {
+  const size_t need = layout_of(p).total;
+  if (ws_bytes < need)
+    return fail(NACL_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", ws_bytes, need);
+  if (!ws) return fail(NACL_ERR_WORKSPACE, "workspace is NULL");
+  if ((uintptr_t)ws % kAlign) return fail(NACL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  return NACL_OK;
+}
+
+int check_select_counts(const nacl_problem* p, int32_t C, int32_t Cr, int32_t sampling) {
+  if (C < 0 || C > p->L) return fail(NACL_ERR_INVALID_ARG, "C must lie in [0, L] (got %d)", C);
+  if (Cr < 0) return fail(NACL_ERR_INVALID_ARG, "Cr must be >= 0 (got %d)", Cr);
+  if ((int64_t)p->n_protect + Cr > C)
+    return fail(NACL_ERR_INVALID_ARG, "n_protect + Cr = %lld exceeds C = %d",
+                (long long)p->n_protect + Cr, C);
+  if (sampling < NACL_SAMPLE_SOFTMAX || sampling > NACL_SAMPLE_UNIFORM)
+    return fail(NACL_ERR_INVALID_ARG, "unknown sampling mode %d", sampling);
+  return NACL_OK;
+}
+
+// Device pointer of the proxy positions; stages the host array into the
+// workspace when the caller gave no device copy.
+int stage_positions(const nacl_problem* p, char* ws, const Layout& l, hipStream_t stream,
+                    const int** out) {
+  if (p->proxy_pos_dev) {
+    *out = p->proxy_pos_dev;
+    return NACL_OK;
+  }
+  int32_t* dst = reinterpret_cast<int32_t*>(ws + l.pos);
+  hipError_t e = hipMemcpyAsync(dst, p->proxy_pos, (size_t)p->P * sizeof(int32_t),
+                                hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return hip_fail(e, "staging proxy positions");
+  *out = dst;
+  return NACL_OK;
+}
+
+int run_score(const nacl_problem* p, const void* q, const void* k, const float* lse, float* scores,
+              char* ws, const Layout& l, const int* pos_dev, hipStream_t stream) {
+  nacl::ScoreLaunch s{};
+  s.args.B = p->B;
+  s.args.H = p->H;
+  s.args.L = p->L;
+  s.args.P = p->P;
+  for (int i = 0; i < 3; ++i) {
+    s.args.qs[i] = p->q_stride[i];
+    s.args.ks[i] = p->k_stride[i];
+  }
+  s.args.pos = pos_dev;
+  s.args.c2 = (float)((double)p->sm_scale * 1.4426950408889634);
+  s.dtype = p->dtype;
+  s.D = p->D;
+  s.q = q;
+  s.k = k;
+  s.run_pass1 = lse == nullptr;
+  const int last = p->proxy_pos[p->P - 1];
+  s.n_chunks1 = last / nacl::kScoreChunkKeys + 1;
+  s.n_chunks2 = (p->L + nacl::kScoreChunkKeys - 1) / nacl::kScoreChunkKeys;
+  s.partials = reinterpret_cast<float2*>(ws + l.part);
+  s.lse2_ws = reinterpret_cast<float*>(ws + l.lse);
+  s.lse_in = lse ? lse : s.lse2_ws;
+  s.lse_mul = lse ? 1.4426950408889634f : 1.0f;
+  s.scores = scores;
+  hipError_t e = nacl::launch_score(s, stream);
+  if (e != hipSuccess) return hip_fail(e, "score kernels");
+  return NACL_OK;
+}
+
+int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr, int32_t sampling,
+               uint64_t seed, uint32_t layer, int32_t* keep, char* ws, const Layout& l,
+               const int* pos_dev, hipStream_t stream) {
+  if (C == 0) return NACL_OK;
+  nacl::SelectLaunch s{};
+  s.B = p->B;
+  s.H = p->H;
+  s.L = p->L;
+  s.P = p->P;
+  s.n_protect = p->n_protect;
+  s.C = C;
+  s.Cr = Cr;
+  s.Cp = C - p->n_protect - Cr;
+  s.sampling = sampling;
+  s.seed = seed;
+  s.layer = layer;
+  s.pos = pos_dev;
+  s.scores = scores;
+  s.keys2 = reinterpret_cast<uint32_t*>(ws + l.keys);
+  s.keep = keep;
+  hipError_t e = nacl::launch_select(s, stream);
+  if (e != hipSuccess) return hip_fail(e, "select kernels");
+  return NACL_OK;
+}
+
+int check_compact_args(const nacl_problem* p, const void* k, const void* v, const int32_t* keep,
+                       int32_t C, const void* k_out, const void* v_out) {
+  if (C < 0 || C > p->L) return fail(NACL_ERR_INVALID_ARG, "C must lie in [0, L] (got %d)", C);
+  if (C == 0) return NACL_OK;
+  if (!k || !v || !keep || !k_out || !v_out)
+    return fail(NACL_ERR_INVALID_ARG, "compaction pointers must be non-NULL");
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out))
+    return fail(NACL_ERR_INVALID_ARG, "K, V, k_out, v_out must be 16-byte aligned");
+  const uintptr_t ob = (uintptr_t)p->B * p->H * C * p->D * elt_bytes(p->dtype);
+  uintptr_t k0, k1, v0, v1;
+  extent(k, p->k_stride, p, k0, k1);
+  extent(v, p->v_stride, p, v0, v1);
+  const uintptr_t ko = (uintptr_t)k_out, vo = (uintptr_t)v_out;
+  const uintptr_t kk0 = (uintptr_t)keep, kk1 = kk0 + (uintptr_t)p->B * p->H * C * 4;
+  if (overlaps(ko, ko + ob, k0, k1) || overlaps(ko, ko + ob, v0, v1) || overlaps(vo, vo + ob, k0, k1) ||
+      overlaps(vo, vo + ob, v0, v1) || overlaps(ko, ko + ob, vo, vo + ob) ||
+      overlaps(ko, ko + ob, kk0, kk1) || overlaps(vo, vo + ob, kk0, kk1))
+    return fail(NACL_ERR_INVALID_ARG, "k_out / v_out overlap an input or each other");
+  return NACL_OK;
+}
+
+int run_compact(const nacl_problem* p, const void* k, const void* v, const int32_t* keep, int32_t C,
+                void* k_out, void* v_out, hipStream_t stream) {
+  if (C == 0) return NACL_OK;
+  nacl::CompactLaunch c{};
+  const int eb = elt_bytes(p->dtype);
+  c.B = p->B;
+  c.H = p->H;
+  c.C = C;
+  c.row_vecs = p->D * eb / 16;
+  for (int i = 0; i < 3; ++i) {
+    c.ks[i] = p->k_stride[i] * eb / 16;
+    c.vs[i] = p->v_stride[i] * eb / 16;
+  }
+  c.k = k;
+  c.v = v;
+  c.keep = keep;
+  c.k_out = k_out;
+  c.v_out = v_out;
+  hipError_t e = nacl::launch_compact(c, stream);
+  if (e != hipSuccess) return hip_fail(e, "compact kernel");
+  return NACL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t nacl_workspace_bytes(const nacl_problem* p) {
+  if (check_problem(p) != NACL_OK) return 0;
+  return layout_of(p).total;
+}
+
+int nacl_score(const nacl_problem* p, const void* q, const void* k, const float* lse, float* scores,
+               void* ws, size_t ws_bytes, void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if (!q || !k || !scores) return fail(NACL_ERR_INVALID_ARG, "q, k and scores must be non-NULL");
+  if (!aligned16(q) || !aligned16(k)) return fail(NACL_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+  if ((st = check_ws(p, ws, ws_bytes))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Layout l = layout_of(p);
+  const int* pos_dev = nullptr;
+  if ((st = stage_positions(p, static_cast<char*>(ws), l, s, &pos_dev))) return st;
+  return run_score(p, q, k, lse, scores, static_cast<char*>(ws), l, pos_dev, s);
+}
+
+int nacl_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr, int32_t sampling,
+                uint64_t seed, uint32_t layer, int32_t* keep_idx, void* ws, size_t ws_bytes,
+                void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if ((st = check_select_counts(p, C, Cr, sampling))) return st;
+  if (C > 0 && (!scores || !keep_idx))
+    return fail(NACL_ERR_INVALID_ARG, "scores and keep_idx must be non-NULL");
+  if ((st = check_ws(p, ws, ws_bytes))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Layout l = layout_of(p);
+  const int* pos_dev = nullptr;
+  if ((st = stage_positions(p, static_cast<char*>(ws), l, s, &pos_dev))) return st;
+  return run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, static_cast<char*>(ws), l,
+                    pos_dev, s);
+}
+
+int nacl_compact(const nacl_problem* p, const void* k, const void* v, const int32_t* keep_idx,
+                 int32_t C, void* k_out, void* v_out, void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out))) return st;
+  return run_compact(p, k, v, keep_idx, C, k_out, v_out, static_cast<hipStream_t>(stream));
+}
+
+int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* v, int32_t C,
+               int32_t Cr, int32_t sampling, uint64_t seed, uint32_t layer, float* scores,
+               int32_t* keep_idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
+               void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if ((st = check_select_counts(p, C, Cr, sampling))) return st;
+  if (!q || !scores) return fail(NACL_ERR_INVALID_ARG, "q and scores must be non-NULL");
+  if (!aligned16(q)) return fail(NACL_ERR_INVALID_ARG, "q must be 16-byte aligned");
+  if (C > 0 && !keep_idx) return fail(NACL_ERR_INVALID_ARG, "keep_idx must be non-NULL");
+  if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out))) return st;
+  if (!k) return fail(NACL_ERR_INVALID_ARG, "k must be non-NULL");
+  if ((st = check_ws(p, ws, ws_bytes))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Layout l = layout_of(p);
+  char* w = static_cast<char*>(ws);
+  const int* pos_dev = nullptr;
+  if ((st = stage_positions(p, w, l, s, &pos_dev))) return st;
+  if ((st = run_score(p, q, k, nullptr, scores, w, l, pos_dev, s))) return st;
+  if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s))) return st;
+  return run_compact(p, k, v, keep_idx, C, k_out, v_out, s);
+}
+
+const char* nacl_status_string(int status) {
+  switch (status) {
+    case NACL_OK: return "ok";
+    case NACL_ERR_INVALID_ARG: return "invalid argument";
+    case NACL_ERR_UNSUPPORTED: return "unsupported";
+    case NACL_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case NACL_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* nacl_last_error_detail(void) { return g_detail; }
+
+int nacl_version(void) { return NACL_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,36 @@
+// Device-side helpers shared by the eviction kernels (gfx950 / CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nacl {
+
+constexpr int kWave = 64;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// exp2 on the transcendental unit (v_exp_f32).  Arguments far below -126
+// return 0; the scores never need values that small.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Order-preserving map of binary32 to uint32: a < b (as floats, no NaNs)
+// iff ord(a) < ord(b) (as unsigned).  0 is below every finite value and
+// serves as the "excluded" sentinel in selections.
+__device__ __forceinline__ uint32_t float_order_key(float f) {
+  uint32_t b = __float_as_uint(f);
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Merge two online-softmax partials (m, s) meaning s * 2^m, in base 2.
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  float mn = fmaxf(m, m2);
+  float a = (m == -INFINITY) ? 0.f : s * fast_exp2(m - mn);
+  float b = (m2 == -INFINITY) ? 0.f : s2 * fast_exp2(m2 - mn);
+  m = mn;
+  s = a + b;
+}
+
+}  // namespace nacl

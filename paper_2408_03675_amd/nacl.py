@@ -1,0 +1,226 @@
+"""Python binding of libnacl.so (the C ABI declared in include/nacl.h).
+
+Argument marshalling only: every step of the eviction runs in the library's
+HIP kernels.  torch tensors provide device memory and the stream.  If the
+built library is missing, importing works but every call raises; there is no
+CPU fallback.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libnacl.so")
+
+NACL_OK = 0
+NACL_ERR_INVALID_ARG = 1
+NACL_ERR_UNSUPPORTED = 2
+NACL_ERR_WORKSPACE = 3
+NACL_ERR_HIP = 4
+
+NACL_F32 = 0
+NACL_BF16 = 1
+
+SAMPLE_SOFTMAX = 0
+SAMPLE_PROPORTIONAL = 1
+SAMPLE_UNIFORM = 2
+
+EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_evict",
+            "nacl_status_string", "nacl_last_error_detail", "nacl_version")
+
+
+class NaclError(RuntimeError):
+    def __init__(self, status, detail):
+        super().__init__(f"nacl status {status}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [
+        ("B", ctypes.c_int32), ("H", ctypes.c_int32), ("L", ctypes.c_int32), ("D", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("P", ctypes.c_int32), ("n_protect", ctypes.c_int32),
+        ("sm_scale", ctypes.c_float),
+        ("q_stride", ctypes.c_int64 * 3), ("k_stride", ctypes.c_int64 * 3),
+        ("v_stride", ctypes.c_int64 * 3),
+        ("proxy_pos", ctypes.POINTER(ctypes.c_int32)),
+        ("proxy_pos_dev", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def load_library(path=LIB_PATH):
+    """Loads libnacl.so once and declares the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2408_03675_amd.build`")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER(_Problem)
+    vp, sz, i32, u32, u64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64
+    lib.nacl_workspace_bytes.argtypes = [P]
+    lib.nacl_workspace_bytes.restype = sz
+    lib.nacl_score.argtypes = [P, vp, vp, vp, vp, vp, sz, vp]
+    lib.nacl_score.restype = ctypes.c_int
+    lib.nacl_select.argtypes = [P, vp, i32, i32, i32, u64, u32, vp, vp, sz, vp]
+    lib.nacl_select.restype = ctypes.c_int
+    lib.nacl_compact.argtypes = [P, vp, vp, vp, i32, vp, vp, vp]
+    lib.nacl_compact.restype = ctypes.c_int
+    lib.nacl_evict.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, vp, sz, vp]
+    lib.nacl_evict.restype = ctypes.c_int
+    lib.nacl_status_string.argtypes = [ctypes.c_int]
+    lib.nacl_status_string.restype = ctypes.c_char_p
+    lib.nacl_last_error_detail.argtypes = []
+    lib.nacl_last_error_detail.restype = ctypes.c_char_p
+    lib.nacl_version.argtypes = []
+    lib.nacl_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != NACL_OK:
+        lib = load_library()
+        raise NaclError(status, lib.nacl_last_error_detail().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _strides(t):
+    if t.dim() != 4 or t.stride(3) != 1:
+        raise ValueError("Q/K/V must be [B, H, L, D] with a contiguous last dimension")
+    return tuple(int(s) for s in t.stride()[:3])
+
+
+class Problem:
+    """nacl_problem for one layer, with its host proxy-position array kept
+    alive.  `dtype` is "bf16" or "f32"."""
+
+    def __init__(self, B, H, L, D, dtype, proxy_pos, n_protect=None, sm_scale=None,
+                 q_stride=None, k_stride=None, v_stride=None, proxy_pos_dev=None):
+        pos = [int(x) for x in proxy_pos]
+        self._pos = (ctypes.c_int32 * max(1, len(pos)))(*pos)
+        self.proxy_pos = pos
+        dense = (H * L * D, L * D, D)
+        s = _Problem()
+        s.B, s.H, s.L, s.D = B, H, L, D
+        s.dtype = NACL_F32 if dtype in ("f32", torch.float32) else NACL_BF16
+        s.P = len(pos)
+        s.n_protect = len(pos) if n_protect is None else int(n_protect)
+        s.sm_scale = float(sm_scale) if sm_scale else 1.0 / (D ** 0.5)
+        s.q_stride[:] = q_stride or dense
+        s.k_stride[:] = k_stride or dense
+        s.v_stride[:] = v_stride or dense
+        s.proxy_pos = ctypes.cast(self._pos, ctypes.POINTER(ctypes.c_int32))
+        self._pos_dev = proxy_pos_dev
+        s.proxy_pos_dev = None if proxy_pos_dev is None else proxy_pos_dev.data_ptr()
+        self.c = s
+
+    @classmethod
+    def from_tensors(cls, q, k, v, proxy_pos, n_protect=None, sm_scale=None, proxy_pos_dev=None):
+        B, H, L, D = k.shape
+        return cls(B, H, L, D, k.dtype, proxy_pos, n_protect, sm_scale,
+                   _strides(q), _strides(k), _strides(v), proxy_pos_dev)
+
+    @property
+    def B(self):
+        return self.c.B
+
+    @property
+    def H(self):
+        return self.c.H
+
+    @property
+    def L(self):
+        return self.c.L
+
+    @property
+    def D(self):
+        return self.c.D
+
+    @property
+    def torch_dtype(self):
+        return torch.float32 if self.c.dtype == NACL_F32 else torch.bfloat16
+
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def workspace_bytes(prob):
+    return int(load_library().nacl_workspace_bytes(prob.ref()))
+
+
+def workspace(prob, device="cuda"):
+    n = workspace_bytes(prob)
+    if n == 0:
+        lib = load_library()
+        raise NaclError(NACL_ERR_INVALID_ARG, lib.nacl_last_error_detail().decode())
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def score(prob, q, k, ws, lse=None, out=None):
+    """F [B, H, L] fp32 (Section 5.1).  lse: optional [B, H, P] natural
+    log-sum-exp from the caller."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=k.device)
+    _check(lib.nacl_score(prob.ref(), _ptr(q), _ptr(k), _ptr(lse), _ptr(out), _ptr(ws),
+                          ws.numel(), _stream(k.device)))
+    return out
+
+
+def select(prob, scores, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=None, out=None):
+    """keep_idx [B, H, C] int32, ascending (Sections 5.1-5.2, Algorithm 1)."""
+    lib = load_library()
+    if out is None:
+        out = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=scores.device)
+    _check(lib.nacl_select(prob.ref(), _ptr(scores), int(C), int(Cr), int(sampling), int(seed),
+                           int(layer), _ptr(out), _ptr(ws), 0 if ws is None else ws.numel(),
+                           _stream(scores.device)))
+    return out
+
+
+def compact(prob, k, v, keep_idx, k_out=None, v_out=None):
+    """K', V' [B, H, C, D] (Section 3)."""
+    lib = load_library()
+    C = keep_idx.shape[-1]
+    if k_out is None:
+        k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=k.device)
+    if v_out is None:
+        v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=v.device)
+    _check(lib.nacl_compact(prob.ref(), _ptr(k), _ptr(v), _ptr(keep_idx), int(C), _ptr(k_out),
+                            _ptr(v_out), _stream(k.device)))
+    return k_out, v_out
+
+
+def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=None,
+          scores=None, keep_idx=None, k_out=None, v_out=None):
+    """score -> select -> compact on the current stream.  Returns
+    (scores, keep_idx, k_out, v_out)."""
+    lib = load_library()
+    dev = k.device
+    if ws is None:
+        ws = workspace(prob, dev)
+    if scores is None:
+        scores = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=dev)
+    if keep_idx is None:
+        keep_idx = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=dev)
+    if k_out is None:
+        k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=dev)
+    if v_out is None:
+        v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=dev)
+    _check(lib.nacl_evict(prob.ref(), _ptr(q), _ptr(k), _ptr(v), int(C), int(Cr), int(sampling),
+                          int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(k_out),
+                          _ptr(v_out), _ptr(ws), ws.numel(), _stream(dev)))
+    return scores, keep_idx, k_out, v_out

@@ -1,0 +1,233 @@
+"""GPU parity: the HIP library through its C ABI against the CPU oracle.
+
+Small problems run whole through the oracle (several tiles, ragged tails,
+scattered and multi-group proxies, fp32 and bf16, D = 64 and 128, strided
+inputs).  Bars: scores within 1e-3 relative; isolated selection on identical
+fp32 scores exactly equal; end-to-end keep sets equal up to near-ties;
+compacted rows bit-exact.
+"""
+
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import (SAMPLE_PROPORTIONAL, SAMPLE_SOFTMAX, SAMPLE_UNIFORM, compact as o_compact,
+                    proxy_scores, select_head)
+from synth import WORKLOADS, custom, make_layer
+from tests._parity import (check_keep_near, check_keep_valid, check_rows_for_common,
+                           check_scores)
+
+pytestmark = pytest.mark.gpu
+
+nacl = pytest.importorskip("paper_2408_03675_amd.nacl")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    nacl.load_library()
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy() if t.dtype == torch.bfloat16 else t.detach().cpu().numpy()
+
+
+def _layer(w, device="cuda"):
+    q, k, v = make_layer(w, 0, device=device)
+    return q, k, v
+
+
+SCORE_CASES = [
+    # name, B, H, L, D, dtype, positions
+    ("f32_d64_suffix", 1, 4, 2048, 64, "f32", list(range(2016, 2048))),
+    ("bf16_d128_ragged", 2, 3, 1000, 128, "bf16", list(range(900, 1000))),
+    ("bf16_d64_scattered", 2, 2, 1037, 64, "bf16", [0, 5, 17, 300, 301, 302, 640, 1000, 1036]),
+    ("f32_d128_scattered", 1, 2, 777, 128, "f32", sorted(set(range(3, 777, 21)))),
+    ("bf16_all_tokens", 1, 2, 96, 64, "bf16", list(range(96))),
+    ("bf16_multigroup", 1, 2, 530, 128, "bf16", list(range(330, 530))),
+    ("f32_single_proxy_mid", 1, 1, 2049, 128, "f32", [1500]),
+    ("bf16_len1", 1, 1, 1, 64, "bf16", [0]),
+    ("bf16_len17", 2, 1, 17, 128, "bf16", [16]),
+]
+
+
+@pytest.mark.parametrize("case", SCORE_CASES, ids=[c[0] for c in SCORE_CASES])
+def test_score_matches_oracle(case):
+    name, B, H, L, D, dt, pos = case
+    _say("score case", name)
+    w = custom(name, B, H, L, D, len(pos), dtype=dt, data_seed=zlib.crc32(name.encode()) % 1000)
+    q, k, v = make_layer(w, 0, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, pos)
+    ws = nacl.workspace(prob)
+    F = nacl.score(prob, q, k, ws)
+    torch.cuda.synchronize()
+    Fr, _ = proxy_scores(_np(q), _np(k), pos, prob.c.sm_scale)
+    rel = check_scores(F.cpu().numpy(), Fr, name)
+    np.testing.assert_allclose(F.cpu().numpy().astype(np.float64).sum(-1), len(pos), rtol=1e-5)
+    _say("  max rel err", rel)
+
+
+def test_score_strided_inputs():
+    """Q, K, V as [B, H, L, D] views of [B, L, H, D] buffers."""
+    B, H, L, D = 2, 4, 700, 128
+    g = torch.Generator(device="cuda").manual_seed(7)
+    base = torch.randn((3, B, L, H, D), generator=g, device="cuda").to(torch.bfloat16)
+    q, k, v = (base[i].permute(0, 2, 1, 3) for i in range(3))
+    pos = list(range(650, 700))
+    prob = nacl.Problem.from_tensors(q, k, v, pos)
+    ws = nacl.workspace(prob)
+    F = nacl.score(prob, q, k, ws)
+    Fr, _ = proxy_scores(_np(q), _np(k), pos, prob.c.sm_scale)
+    check_scores(F.cpu().numpy(), Fr, "strided")
+
+
+def test_score_with_caller_lse():
+    """With the caller's log-sum-exp (Appendix A.7, Algorithm 2) only the
+    column reduction runs and gives the same scores."""
+    w = custom("lse", 1, 3, 1500, 128, 40, dtype="bf16", data_seed=3)
+    q, k, v = make_layer(w, 0, device="cuda")
+    pos = w.proxy_pos
+    prob = nacl.Problem.from_tensors(q, k, v, pos)
+    Fr, lse = proxy_scores(_np(q), _np(k), pos, prob.c.sm_scale)
+    lse_t = torch.from_numpy(lse.astype(np.float32)).cuda()
+    F = nacl.score(prob, q, k, nacl.workspace(prob), lse=lse_t)
+    check_scores(F.cpu().numpy(), Fr, "caller lse")
+
+
+def test_score_config_small_and_longbench():
+    for key in ("small_f32", "longbench_4k"):
+        w = WORKLOADS[key]
+        _say("score workload", key)
+        q, k, v = _layer(w)
+        prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=w.scale)
+        F = nacl.score(prob, q, k, nacl.workspace(prob))
+        Fr, _ = proxy_scores(_np(q), _np(k), w.proxy_pos, w.scale)
+        check_scores(F.cpu().numpy(), Fr, key)
+
+
+SELECT_CASES = [
+    # name, L, P, n_protect, C, Cr, mode, ties
+    ("softmax_basic", 2048, 32, 32, 409, 245, SAMPLE_SOFTMAX, False),
+    ("proportional", 3001, 50, 50, 600, 200, SAMPLE_PROPORTIONAL, False),
+    ("uniform", 1000, 10, 10, 300, 150, SAMPLE_UNIFORM, False),
+    ("no_random", 4096, 64, 64, 819, 0, SAMPLE_SOFTMAX, False),
+    ("all_random", 4096, 64, 64, 819, 755, SAMPLE_SOFTMAX, False),
+    ("no_protect", 1500, 20, 0, 300, 100, SAMPLE_SOFTMAX, False),
+    ("keep_all", 777, 7, 7, 777, 300, SAMPLE_SOFTMAX, False),
+    ("keep_protected_only", 512, 16, 16, 16, 0, SAMPLE_SOFTMAX, False),
+    ("ties_heavy", 5000, 8, 8, 1000, 300, SAMPLE_SOFTMAX, True),
+    ("ties_uniform", 2500, 8, 4, 700, 100, SAMPLE_UNIFORM, True),
+    ("tiny", 5, 1, 1, 3, 1, SAMPLE_SOFTMAX, False),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=[c[0] for c in SELECT_CASES])
+def test_select_exact_on_identical_scores(case):
+    name, L, P, n_protect, C, Cr, mode, ties = case
+    _say("select case", name)
+    B, H = 2, 3
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    F = rng.gamma(0.3, 1.0 / L, size=(B, H, L))
+    if ties:
+        F = np.round(F * L * 4) / (L * 4)
+    F32 = F.astype(np.float32)
+    pos = list(range(L - P, L))
+    prob = nacl.Problem(B, H, L, 128, "bf16", pos, n_protect=n_protect)
+    ws = nacl.workspace(prob)
+    keep = nacl.select(prob, torch.from_numpy(F32).cuda(), C, Cr, mode, seed=1234, layer=5, ws=ws)
+    keep = keep.cpu().numpy()
+    for b in range(B):
+        for h in range(H):
+            ref = select_head(F32[b, h], pos, n_protect, C, Cr, mode, 1234, 5, b, h)
+            assert np.array_equal(keep[b, h], ref["keep"]), (name, b, h)
+
+
+def test_select_full_length_limit_head():
+    """A long head (131072 tokens, the 128k workload's length)."""
+    L, P, C, Cr = 131072, 512, 26214, 15728
+    rng = np.random.default_rng(9)
+    F32 = rng.gamma(0.5, 512.0 / L / 0.5, size=(1, 2, L)).astype(np.float32)
+    pos = list(range(L - P, L))
+    prob = nacl.Problem(1, 2, L, 128, "bf16", pos)
+    keep = nacl.select(prob, torch.from_numpy(F32).cuda(), C, Cr, SAMPLE_SOFTMAX, 0, 0,
+                       ws=nacl.workspace(prob)).cpu().numpy()
+    for h in range(2):
+        ref = select_head(F32[0, h], pos, P, C, Cr, SAMPLE_SOFTMAX, 0, 0, 0, h)
+        assert np.array_equal(keep[0, h], ref["keep"])
+
+
+@pytest.mark.parametrize("dt,D", [("bf16", 128), ("bf16", 64), ("f32", 64), ("f32", 128)])
+def test_compact_bit_exact(dt, D):
+    B, H, L, C = 2, 3, 1000, 211
+    w = custom("cmp", B, H, L, D, 4, dtype=dt, data_seed=D)
+    q, k, v = make_layer(w, 0, device="cuda")
+    rng = np.random.default_rng(D)
+    idx = np.sort(np.stack([[rng.choice(L, C, replace=False) for _ in range(H)] for _ in range(B)]), -1)
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos)
+    ko, vo = nacl.compact(prob, k, v, torch.from_numpy(idx.astype(np.int32)).cuda())
+    kr, vr = o_compact(k.cpu().view(torch.int16 if dt == "bf16" else torch.int32).numpy(),
+                       v.cpu().view(torch.int16 if dt == "bf16" else torch.int32).numpy(), idx)
+    view = torch.int16 if dt == "bf16" else torch.int32
+    assert np.array_equal(ko.cpu().view(view).numpy(), kr)
+    assert np.array_equal(vo.cpu().view(view).numpy(), vr)
+
+
+def _evict_and_compare(w, layer=0, heads=None, keep_frac=None, random_share=None, label=""):
+    q, k, v = make_layer(w, layer, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=w.scale)
+    ws = nacl.workspace(prob)
+    F, keep, ko, vo = nacl.evict(prob, q, k, v, w.C, w.Cr, SAMPLE_SOFTMAX, w.rng_seed, layer, ws=ws)
+    torch.cuda.synchronize()
+    F = F.cpu().numpy()
+    keep = keep.cpu().numpy()
+    check_keep_valid(keep, w.L, w.C, w.proxy_pos[w.P - w.n_protect:])
+    np.testing.assert_allclose(F.astype(np.float64).sum(-1), w.P, rtol=1e-5)
+    if heads is None:
+        heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+    view = torch.int16 if w.dtype == "bf16" else torch.int32
+    n_diff = 0
+    for (b, h) in heads:
+        qh = _np(q[b:b + 1, h:h + 1])
+        kh = _np(k[b:b + 1, h:h + 1])
+        Fr, _ = proxy_scores(qh, kh, w.proxy_pos, w.scale)
+        check_scores(F[b, h], Fr[0, 0], f"{label} F b={b} h={h}")
+        Fr32 = Fr[0, 0].astype(np.float32)
+        ref = select_head(Fr32, w.proxy_pos, w.n_protect, w.C, w.Cr, SAMPLE_SOFTMAX, w.rng_seed,
+                          layer, b, h)
+        n_diff += check_keep_near(keep[b, h], ref, Fr32, w.Cr, f"{label} keep b={b} h={h}")
+        kbits = k[b, h].cpu().view(view).numpy()
+        vbits = v[b, h].cpu().view(view).numpy()
+        check_rows_for_common(keep[b, h], ko[b, h].cpu().view(view).numpy(), ref["keep"],
+                              kbits[ref["keep"]], f"{label} K' b={b} h={h}")
+        check_rows_for_common(keep[b, h], vo[b, h].cpu().view(view).numpy(), ref["keep"],
+                              vbits[ref["keep"]], f"{label} V' b={b} h={h}")
+    _say(f"  {label}: {len(heads)} heads compared, {n_diff} near-tie differences")
+
+
+def test_evict_small_f32_all_heads():
+    _evict_and_compare(WORKLOADS["small_f32"], label="small_f32")
+
+
+def test_evict_longbench_all_heads():
+    _evict_and_compare(WORKLOADS["longbench_4k"], label="longbench_4k")
+
+
+def test_evict_is_deterministic():
+    w = WORKLOADS["longbench_4k"]
+    q, k, v = make_layer(w, 0, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos)
+    ws = nacl.workspace(prob)
+    a = [t.clone() for t in nacl.evict(prob, q, k, v, w.C, w.Cr, 0, 7, 3, ws=ws)]
+    b = nacl.evict(prob, q, k, v, w.C, w.Cr, 0, 7, 3, ws=ws)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    c = nacl.evict(prob, q, k, v, w.C, w.Cr, 0, 7, 4, ws=ws)
+    assert not torch.equal(a[1], c[1])
