@@ -12,6 +12,8 @@
 #include "../../include/nacl.h"
 #include "internal.h"
 
+#include <algorithm>
+
 namespace {
 
 thread_local char g_detail[512] = "";
@@ -34,21 +36,25 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
 
 struct Layout {
-  size_t pos, lse, part, keys, total;
-  int n_chunks_max;
+  size_t cnt, pos, lse, part, keys, total;
+  int n_chunks;
 };
+
+constexpr int kCounterHeader = 64;  // queue + status words, padded to 256 bytes
 
 Layout layout_of(const nacl_problem* p) {
   Layout l;
   const size_t BH = (size_t)p->B * p->H;
-  l.n_chunks_max = (p->L + nacl::kScoreChunkKeys - 1) / nacl::kScoreChunkKeys;
+  l.n_chunks = (p->L + nacl::kScoreChunkKeys - 1) / nacl::kScoreChunkKeys;
   size_t off = 0;
+  l.cnt = off;
+  off += align_up((kCounterHeader + BH) * sizeof(uint32_t));
   l.pos = off;
   off += align_up((size_t)p->P * sizeof(int32_t));
   l.lse = off;
   off += align_up(BH * p->P * sizeof(float));
   l.part = off;
-  off += align_up(BH * l.n_chunks_max * p->P * sizeof(float2));
+  off += align_up(BH * l.n_chunks * p->P * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
   l.total = off;
@@ -100,6 +106,10 @@ int check_problem(const nacl_problem* p) {
         return fail(NACL_ERR_INVALID_ARG, "%s[%d] * element size must be a multiple of 16 bytes",
                     names[t], i);
     }
+  // The score kernel addresses one head's K rows through a buffer
+  // descriptor with 32-bit byte offsets.
+  if ((int64_t)(p->L - 1) * p->k_stride[2] * eb + (int64_t)p->D * eb >= ((int64_t)1 << 31))
+    return fail(NACL_ERR_UNSUPPORTED, "one head's K rows span 2 GiB or more (L * k_stride[2])");
   return NACL_OK;
 }
 
@@ -141,6 +151,15 @@ int stage_positions(const nacl_problem* p, char* ws, const Layout& l, hipStream_
   return NACL_OK;
 }
 
+// Heads per scheduling group: the largest divisor of B*H whose items fill
+// about one round of resident work-groups.
+int heads_per_group(int BH, int n_chunks, int target_items) {
+  int best = 1;
+  for (int g = 1; g <= BH; ++g)
+    if (BH % g == 0 && (int64_t)g * n_chunks <= target_items) best = g;
+  return best;
+}
+
 int run_score(const nacl_problem* p, const void* q, const void* k, const float* lse, float* scores,
               char* ws, const Layout& l, const int* pos_dev, hipStream_t stream) {
   nacl::ScoreLaunch s{};
@@ -153,22 +172,36 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
     s.args.ks[i] = p->k_stride[i];
   }
   s.args.pos = pos_dev;
+  s.args.p_last = p->proxy_pos[p->P - 1];
   s.args.c2 = (float)((double)p->sm_scale * 1.4426950408889634);
   s.dtype = p->dtype;
   s.D = p->D;
   s.q = q;
   s.k = k;
-  s.run_pass1 = lse == nullptr;
-  const int last = p->proxy_pos[p->P - 1];
-  s.n_chunks1 = last / nacl::kScoreChunkKeys + 1;
-  s.n_chunks2 = (p->L + nacl::kScoreChunkKeys - 1) / nacl::kScoreChunkKeys;
-  s.partials = reinterpret_cast<float2*>(ws + l.part);
-  s.lse2_ws = reinterpret_cast<float*>(ws + l.lse);
-  s.lse_in = lse ? lse : s.lse2_ws;
-  s.lse_mul = lse ? 1.4426950408889634f : 1.0f;
-  s.scores = scores;
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return fail(NACL_ERR_HIP, "querying the device");
+  const int BH = p->B * p->H;
+  nacl::ScoreSched& sc = s.sched;
+  sc.n_chunks = l.n_chunks;
+  sc.heads_per_group = heads_per_group(BH, l.n_chunks, NACL_SCORE_GROUP_ITEMS_PER_CU * cus);
+  sc.n_groups = BH / sc.heads_per_group;
+  sc.lag = std::min(NACL_SCORE_LAG, sc.n_groups);
+  sc.lse_given = lse != nullptr;
+  sc.total_items = (sc.lse_given ? 1 : 2) * BH * l.n_chunks;
+  uint32_t* words = reinterpret_cast<uint32_t*>(ws + l.cnt);
+  sc.queue = words;
+  sc.status = words + 1;
+  sc.head_cnt = words + kCounterHeader;
+  sc.partials = reinterpret_cast<float2*>(ws + l.part);
+  sc.lse2 = reinterpret_cast<float*>(ws + l.lse);
+  sc.lse_in = lse;
+  sc.lse_mul = 1.4426950408889634f;
+  sc.scores = scores;
+  s.n_counter_words = kCounterHeader + BH;
   hipError_t e = nacl::launch_score(s, stream);
-  if (e != hipSuccess) return hip_fail(e, "score kernels");
+  if (e != hipSuccess) return hip_fail(e, "score kernel");
   return NACL_OK;
 }
 

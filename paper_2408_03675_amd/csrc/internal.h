@@ -8,29 +8,64 @@
 
 namespace nacl {
 
-// Keys per score work-group = kScoreTilesPerWave * 4 waves * 16 keys.
-constexpr int kScoreTilesPerWave = 8;
-constexpr int kScoreChunkKeys = kScoreTilesPerWave * 4 * 16;
+// Score kernel shape.  A work item spans 2 key groups x kScoreTilesPerWave
+// tiles of 16 keys; kScoreWavesPerSimd is the occupancy the register
+// allocation targets.
+#ifndef NACL_SCORE_TPW
+#define NACL_SCORE_TPW 32
+#endif
+#ifndef NACL_SCORE_WAVES
+#define NACL_SCORE_WAVES 3
+#endif
+#ifndef NACL_SCORE_KEY_GROUPS
+#define NACL_SCORE_KEY_GROUPS 2
+#endif
+// Scheduling: pass-1 items of about GROUP_ITEMS_PER_CU * CUs items form a
+// head group; pass-2 items of group g follow pass-1 items of group g + LAG.
+#ifndef NACL_SCORE_GROUP_ITEMS_PER_CU
+#define NACL_SCORE_GROUP_ITEMS_PER_CU 2
+#endif
+#ifndef NACL_SCORE_LAG
+#define NACL_SCORE_LAG 2
+#endif
+constexpr int kScoreTilesPerWave = NACL_SCORE_TPW;
+constexpr int kScoreWavesPerSimd = NACL_SCORE_WAVES;
+constexpr int kScoreKeyGroups = NACL_SCORE_KEY_GROUPS;
+constexpr int kScoreChunkKeys = kScoreTilesPerWave * kScoreKeyGroups * 16;
 
 struct ScoreArgs {
   int B, H, L, P;
   int64_t qs[3], ks[3];
   const int* pos;   // device, P entries
+  int p_last;       // pos[P - 1]
   float c2;         // sm_scale * log2(e)
+};
+
+// Work queue of the persistent score kernel (see score.hip).
+struct ScoreSched {
+  int n_chunks;          // key chunks per head (kScoreChunkKeys keys each)
+  int heads_per_group;   // heads per scheduling group
+  int n_groups;          // B*H / heads_per_group
+  int lag;               // pass-2 items of group g follow pass-1 items of group g + lag
+  int total_items;
+  int lse_given;         // 1: the caller supplied the log-sum-exp, only pass 2 runs
+  uint32_t* queue;       // workspace counter words: queue, status, then per-head counters
+  uint32_t* status;      // bit 0 set if a pass-2 wait hit its spin limit (never expected)
+  uint32_t* head_cnt;    // [B*H]
+  float2* partials;      // [B*H, n_chunks, P] base-2 (max, sum)
+  float* lse2;           // [B*H, P] base-2 log-sum-exp
+  const float* lse_in;   // caller's log-sum-exp when lse_given
+  float lse_mul;         // log2(e) for a natural log-sum-exp
+  float* scores;         // [B*H, L]
 };
 
 struct ScoreLaunch {
   ScoreArgs args;
+  ScoreSched sched;
   int dtype, D;
   const void* q;
   const void* k;
-  bool run_pass1;        // false: caller supplied the log-sum-exp
-  int n_chunks1, n_chunks2;
-  float2* partials;      // workspace [B*H, n_chunks1, P]
-  float* lse2_ws;        // workspace [B*H, P], base-2 log-sum-exp
-  const float* lse_in;   // what pass 2 reads (lse2_ws or the caller's)
-  float lse_mul;         // 1 for base 2, log2(e) for natural log-sum-exp
-  float* scores;         // [B*H, L]
+  int n_counter_words;   // words zeroed before the launch, from sched.queue
 };
 
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream);
