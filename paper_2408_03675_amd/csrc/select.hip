@@ -9,8 +9,8 @@
 //   keep     Pi | u_score | u_random, ascending, exactly C entries
 //
 // Both top-k searches are exact radix selects over order-preserving uint32
-// keys (four 8-bit digits, most significant first): each digit pass builds a
-// 256-bin histogram of the keys that still match the chosen prefix and picks
+// keys (12-, 12- and 8-bit digits, most significant first): each digit pass
+// builds a histogram of the keys that still match the chosen prefix and picks
 // the digit where the count from the top reaches k.  That yields the k-th
 // largest key T and how many keys equal to T to take; a block-wide ordered
 // scan then hands those to the lowest indices.  Set membership lives in LDS
@@ -84,76 +84,105 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scan_buf) {
 }
 
 struct SelScratch {
-  uint32_t* hist;   // kSelWaves * 256
-  uint32_t* tot;    // 256
+  uint32_t* hist;   // kHistBins
   uint32_t* scan;   // 2 * kSelWaves
   uint32_t* shv;    // 4
 };
 
-// k-th largest key (1 <= k <= number of keys) and the number of keys equal to
-// it that belong to the top k.
+// Radix select digits, most significant first: 12 + 12 + 8 bits.  The wide
+// first digit spreads even tightly clustered keys (scores within a few
+// binades) over many counters, so the shared histogram's atomics rarely
+// collide; later passes only count keys that match the chosen prefix.
+constexpr int kHistBins = 4096;
+constexpr int kDigitShift[3] = {20, 8, 0};
+constexpr int kDigitBits[3] = {12, 12, 8};
+
+// k-th largest key T (1 <= k <= number of keys), the number `need` of keys
+// equal to T that belong to the top k, and the number n_eq of keys equal to T.
 template <class Get>
 __device__ void radix_select(const Get& get, int L, uint32_t k, const SelScratch& s, uint32_t& T,
-                             uint32_t& need) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+                             uint32_t& need, uint32_t& n_eq) {
+  const int tid = threadIdx.x;
   uint32_t prefix = 0u, kr = k;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    const uint32_t hm = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + 8));
-    for (int i = tid; i < kSelWaves * 256; i += kSelThreads) s.hist[i] = 0u;
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = kDigitShift[pass];
+    const int nbins = 1 << kDigitBits[pass];
+    const uint32_t dmask = (uint32_t)nbins - 1u;
+    const uint32_t hm = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + kDigitBits[pass]));
+    for (int i = tid; i < nbins; i += kSelThreads) s.hist[i] = 0u;
     __syncthreads();
-    uint32_t* hw = s.hist + wave * 256;
-    int run_bin = -1;
-    uint32_t run = 0;
-    for (int j = tid; j < L; j += kSelThreads) {
-      const uint32_t key = get(j);
-      if (((key ^ prefix) & hm) == 0u) {
-        const int bin = (key >> shift) & 255;
-        if (bin != run_bin) {
-          if (run) atomicAdd(&hw[run_bin], run);
-          run_bin = bin;
-          run = 0;
-        }
-        ++run;
+    // Eight keys per thread in flight before their counter updates.
+    for (int j0 = tid; j0 < L; j0 += 8 * kSelThreads) {
+      uint32_t kv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kSelThreads;
+        kv[u] = j < L ? get(j) : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kSelThreads;
+        if (j < L && ((kv[u] ^ prefix) & hm) == 0u) atomicAdd(&s.hist[(kv[u] >> shift) & dmask], 1u);
       }
     }
-    if (run) atomicAdd(&hw[run_bin], run);
     __syncthreads();
-    if (tid < 256) {
-      uint32_t t = 0;
+    // Counts from the top: thread t owns bins nbins-1-4t down to nbins-4-4t.
+    const int per = (nbins + kSelThreads - 1) / kSelThreads;  // 4 or 1
+    uint32_t c[4] = {0u, 0u, 0u, 0u}, local = 0u;
 #pragma unroll
-      for (int w = 0; w < kSelWaves; ++w) t += s.hist[w * 256 + tid];
-      s.tot[tid] = t;
+    for (int qq = 0; qq < 4; ++qq) {
+      const int b = nbins - 1 - per * tid - qq;
+      if (qq < per && b >= 0) c[qq] = s.hist[b];
+      local += c[qq];
     }
-    __syncthreads();
-    if (wave == 0) {
-      uint32_t c[4], local = 0;
-#pragma unroll
-      for (int qq = 0; qq < 4; ++qq) {
-        c[qq] = s.tot[255 - 4 * lane - qq];
-        local += c[qq];
-      }
-      const uint32_t incl = wave_inclusive_scan(local, lane);
-      const uint32_t excl = incl - local;
-      if (excl < kr && kr <= incl) {
-        uint32_t cum = excl;
-        for (int qq = 0; qq < 4; ++qq) {
-          if (cum + c[qq] >= kr) {
-            s.shv[0] = prefix | ((uint32_t)(255 - 4 * lane - qq) << shift);
-            s.shv[1] = kr - cum;
-            break;
-          }
-          cum += c[qq];
+    const uint32_t excl = block_exclusive_scan(local, s.scan);
+    if (excl < kr && kr <= excl + local) {
+      uint32_t cum = excl;
+      for (int qq = 0; qq < per; ++qq) {
+        if (cum + c[qq] >= kr) {
+          s.shv[0] = prefix | ((uint32_t)(nbins - 1 - per * tid - qq) << shift);
+          s.shv[1] = kr - cum;
+          s.shv[2] = c[qq];
+          break;
         }
+        cum += c[qq];
       }
     }
     __syncthreads();
     prefix = s.shv[0];
     kr = s.shv[1];
+    n_eq = s.shv[2];
     __syncthreads();
   }
   T = prefix;
   need = kr;
+}
+
+// Sets, in out_bits, the bit of every token with key >= T: the top k when
+// every key equal to T belongs to it.  Each wave covers 64 consecutive tokens
+// per step and writes their two bitmap words from a ballot.
+template <class Get>
+__device__ void mark_at_least(const Get& get, int L, uint32_t T, uint32_t* out_bits) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int b0 = wave * 64; b0 < L; b0 += 4 * kSelThreads) {
+    bool take[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = b0 + u * kSelThreads + lane;
+      take[u] = j < L && get(j) >= T;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int base = b0 + u * kSelThreads;
+      const uint64_t m = __ballot(take[u]);
+      if (lane == 0 && base < L) {
+        out_bits[base >> 5] |= (uint32_t)m;
+        if (base + 32 < L) out_bits[(base >> 5) + 1] |= (uint32_t)(m >> 32);
+      }
+    }
+  }
+  __syncthreads();
 }
 
 // Sets, in out_bits, the bit of every token with key > T and of the first
@@ -190,17 +219,62 @@ __device__ void mark_top(const Get& get, int L, int nwords, int seg_words, uint3
   __syncthreads();
 }
 
+// The top k of get() into out_bits: ballot marking when every key equal to
+// the k-th largest is kept, the ordered tie scan otherwise.
+template <class Get>
+__device__ void select_top(const Get& get, int L, int nwords, int seg_words, uint32_t k,
+                           const SelScratch& s, uint32_t* out_bits) {
+  uint32_t T, need, n_eq;
+  radix_select(get, L, k, s, T, need, n_eq);
+  if (need == n_eq) mark_at_least(get, L, T, out_bits);
+  else mark_top(get, L, nwords, seg_words, T, need, out_bits, s.scan);
+}
+
+// keys_lds[j] = f(j, src[j]) for the whole head: 16-byte loads, eight per
+// thread in flight (src is 16-byte aligned when L % 4 == 0; otherwise
+// 4-byte loads).
+template <class F>
+__device__ void stage_keys(int L, const uint32_t* src, uint32_t* keys_lds, const F& f) {
+  if ((L & 3) == 0) {
+    const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
+    const int n4 = L >> 2;
+    for (int i0 = threadIdx.x; i0 < n4; i0 += 8 * kSelThreads) {
+      u32x4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * kSelThreads;
+        v[u] = i < n4 ? s4[i] : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * kSelThreads;
+        if (i < n4) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) keys_lds[4 * i + e] = f(4 * i + e, v[u][e]);
+        }
+      }
+    }
+  } else {
+    for (int j = threadIdx.x; j < L; j += kSelThreads) keys_lds[j] = f(j, src[j]);
+  }
+  __syncthreads();
+}
+
+// KEYS_IN_LDS: the head's keys live in LDS (L * 4 bytes), loaded once per
+// selection; otherwise every radix pass re-reads them from global memory
+// (L2-resident) for heads too long for LDS.
+template <bool KEYS_IN_LDS>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
   extern __shared__ uint32_t smem[];
   const int L = a.L;
   const int nwords = (L + 31) / 32;
   const int seg_words = (nwords + kSelThreads - 1) / kSelThreads;
-  uint32_t* prot = smem;
+  uint32_t* keys_lds = smem;
+  uint32_t* prot = smem + (KEYS_IN_LDS ? L : 0);
   uint32_t* sel = prot + nwords;
   SelScratch s;
   s.hist = sel + nwords;
-  s.tot = s.hist + kSelWaves * 256;
-  s.scan = s.tot + 256;
+  s.scan = s.hist + kHistBins;
   s.shv = s.scan + 2 * kSelWaves;
 
   const int tid = threadIdx.x;
@@ -218,49 +292,65 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
     atomicOr(&prot[j >> 5], 1u << (j & 31));
   }
   __syncthreads();
+  auto excluded = [&](int j) -> bool { return (((prot[j >> 5] | sel[j >> 5]) >> (j & 31)) & 1u) != 0u; };
 
   // u_score: top-Cp of F over R.
   if (a.Cp > 0) {
-    auto key1 = [&](int j) -> uint32_t {
-      return ((prot[j >> 5] >> (j & 31)) & 1u) ? 0u : float_order_key(f[j]);
-    };
-    uint32_t T1, need1;
-    radix_select(key1, L, (uint32_t)a.Cp, s, T1, need1);
-    mark_top(key1, L, nwords, seg_words, T1, need1, sel, s.scan);
+    if constexpr (KEYS_IN_LDS) {
+      stage_keys(L, reinterpret_cast<const uint32_t*>(f), keys_lds,
+                 [&](int j, uint32_t bits) { return excluded(j) ? 0u : float_order_key(__uint_as_float(bits)); });
+      select_top([&](int j) { return keys_lds[j]; }, L, nwords, seg_words, (uint32_t)a.Cp, s, sel);
+    } else {
+      select_top([&](int j) { return ((prot[j >> 5] >> (j & 31)) & 1u) ? 0u : float_order_key(f[j]); }, L,
+                 nwords, seg_words, (uint32_t)a.Cp, s, sel);
+    }
   }
 
   // u_random: top-Cr of the Gumbel keys over R \ u_score.
   if (a.Cr > 0) {
-    auto key2 = [&](int j) -> uint32_t {
-      return (((prot[j >> 5] | sel[j >> 5]) >> (j & 31)) & 1u) ? 0u : keys[j];
-    };
-    uint32_t T2, need2;
-    radix_select(key2, L, (uint32_t)a.Cr, s, T2, need2);
-    mark_top(key2, L, nwords, seg_words, T2, need2, sel, s.scan);
+    if constexpr (KEYS_IN_LDS) {
+      stage_keys(L, keys, keys_lds, [&](int j, uint32_t key) { return excluded(j) ? 0u : key; });
+      select_top([&](int j) { return keys_lds[j]; }, L, nwords, seg_words, (uint32_t)a.Cr, s, sel);
+    } else {
+      // Reads sel inside the marking of sel: a token's own bit is read before
+      // its word is updated, and random picks are never excluded tokens.
+      select_top([&](int j) { return excluded(j) ? 0u : keys[j]; }, L, nwords, seg_words, (uint32_t)a.Cr, s,
+                 sel);
+    }
   }
 
-  // keep = Pi | u_score | u_random, written in ascending order.
+  // keep = Pi | u_score | u_random, in ascending order: ranks by an ordered
+  // scan of the bitmap words, the list assembled in LDS (over the keys when
+  // they live there), then copied out with coalesced stores.
   const int w0 = tid * seg_words;
   const int w1 = min(w0 + seg_words, nwords);
   uint32_t cnt = 0;
   for (int w = w0; w < w1; ++w) cnt += __popc(sel[w] | prot[w]);
   uint32_t out = block_exclusive_scan(cnt, s.scan);
   int32_t* keep = a.keep + (int64_t)bh * a.C;
+  int32_t* list = KEYS_IN_LDS ? reinterpret_cast<int32_t*>(keys_lds) : keep;
   for (int w = w0; w < w1; ++w) {
     uint32_t bits = sel[w] | prot[w];
     while (bits) {
       const int bit = __ffs(bits) - 1;
-      if (out < (uint32_t)a.C) keep[out] = w * 32 + bit;  // |keep| == C by construction
+      if (out < (uint32_t)a.C) list[out] = w * 32 + bit;  // |keep| == C by construction
       ++out;
       bits &= bits - 1;
     }
   }
+  if constexpr (KEYS_IN_LDS) {
+    __syncthreads();
+    for (int c = tid; c < a.C; c += kSelThreads) keep[c] = list[c];
+  }
 }
 
-size_t select_lds_bytes(int L) {
+// LDS bytes of select_kernel: bitmaps + histograms (+ keys when in LDS).
+size_t select_lds_bytes(int L, bool keys_in_lds) {
   const size_t nwords = ((size_t)L + 31) / 32;
-  return (2 * nwords + kSelWaves * 256 + 256 + 2 * kSelWaves + 4) * sizeof(uint32_t);
+  return ((keys_in_lds ? (size_t)L : 0) + 2 * nwords + kHistBins + 2 * kSelWaves + 4) * sizeof(uint32_t);
 }
+
+constexpr size_t kMaxLds = 160 * 1024;
 
 hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
   const int BH = a.B * a.H;
@@ -279,13 +369,15 @@ hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const size_t lds = select_lds_bytes(a.L);
+  const bool in_lds = select_lds_bytes(a.L, true) <= kMaxLds;
+  const size_t lds = select_lds_bytes(a.L, in_lds);
+  const void* fn = in_lds ? (const void*)select_kernel<true> : (const void*)select_kernel<false>;
   if (lds > 64 * 1024) {
-    hipError_t e = hipFuncSetAttribute((const void*)select_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(select_kernel, dim3(BH), dim3(kSelThreads), lds, stream, a);
+  if (in_lds) hipLaunchKernelGGL(select_kernel<true>, dim3(BH), dim3(kSelThreads), lds, stream, a);
+  else hipLaunchKernelGGL(select_kernel<false>, dim3(BH), dim3(kSelThreads), lds, stream, a);
   return hipGetLastError();
 }
 
