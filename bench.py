@@ -27,10 +27,18 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 F32_PEAK_TFLOPS = 157.3        # dense fp32 MFMA
 
-# FETCH_SIZE / WRITE_SIZE scale factors and the per-launch traffic of the
-# dominant kernel, from the rocprofv3 counter runs summarised under profiles/.
-# None until measured for the current kernel.
-MEASURED_TRAFFIC = None
+# HBM traffic of the dominant kernel per launch, from two rocprofv3 --pmc runs
+# (FETCH_SIZE, then WRITE_SIZE) scaled by the same counters on a plain copy of
+# known size; summarised under profiles/.  It is reported only while the
+# kernel source hashes to the value it was measured on.
+MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_kernel", "bytes_per_launch": 2234945210,
+                    "source_sha": "57feb1392517442b"}
+
+
+def _source_sha(rel):
+    import hashlib
+    with open(os.path.join(ROOT, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 def log(*a):
@@ -46,7 +54,12 @@ def parse():
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (profiling only)")
     ap.add_argument("--stage-reps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-heads", type=int, default=32)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="run the CPU oracle on whole layers until this much time has passed")
+    ap.add_argument("--probe", choices=["score", "select", "compact", "copy"],
+                    help="run one kernel three times on layer 0 and exit (for rocprofv3 counter runs)")
+    ap.add_argument("--pass-breakdown", action="store_true",
+                    help="also time the score kernel's second pass alone (caller-supplied LSE)")
     return ap.parse_args()
 
 
@@ -64,6 +77,8 @@ def main():
 
     w = WORKLOADS[args.workload]
     layers = args.layers or w.layers
+    if args.probe:
+        layers = 1
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     nacl.load_library()
@@ -85,6 +100,10 @@ def main():
                      torch.empty((w.B, w.H, w.C), dtype=torch.int32, device=dev),
                      torch.empty((w.B, w.H, w.C, w.D), dtype=q0.dtype, device=dev),
                      torch.empty((w.B, w.H, w.C, w.D), dtype=q0.dtype, device=dev)))
+
+    if args.probe:
+        run_probe(args.probe, w, prob, ws, data[0], outs[0])
+        return
 
     def step():
         for l in range(layers):
@@ -111,11 +130,10 @@ def main():
     tok_per_s = w.B * w.L * layers / (ms_per_step / 1e3)
     log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, {ms_per_step / layers * 1e3:.1f} us/layer")
 
-    # Per-kernel durations through the public entry points, timed with events
-    # on the launch stream: score with the caller's log-sum-exp runs only the
-    # column-reduction kernel; without it, pass 1 + combine run too.
-    lse_ws = torch.empty((w.B, w.H, w.P), dtype=torch.float32, device=dev)
-
+    # Per-stage durations through the public entry points, timed with events
+    # on the launch stream.  nacl_score = score_init_kernel (zeroes the work
+    # queue counters, ~5 us) + score_kernel; nacl_select = gumbel_keys_kernel
+    # + select_kernel; nacl_compact = compact_kernel.
     def timed(fn):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         torch.cuda.synchronize()
@@ -125,15 +143,11 @@ def main():
                 fn(l)
         ev[1].record(stream)
         torch.cuda.synchronize()
-        return ev[0].elapsed_time(ev[1]) / (args.stage_reps * layers) * 1e3  # us per launch
+        return ev[0].elapsed_time(ev[1]) / (args.stage_reps * layers) * 1e3  # us per call
 
     def f_score(l):
         q, k, v = data[l]
         nacl.score(prob, q, k, ws, out=outs[l][0])
-
-    def f_pass2(l):
-        q, k, v = data[l]
-        nacl.score(prob, q, k, ws, lse=lse_ws, out=outs[l][0])
 
     def f_select(l):
         nacl.select(prob, outs[l][0], w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, l, ws=ws, out=outs[l][1])
@@ -142,55 +156,60 @@ def main():
         q, k, v = data[l]
         nacl.compact(prob, k, v, outs[l][1], k_out=outs[l][2], v_out=outs[l][3])
 
-    # A finite log-sum-exp for the pass-2-only timing: 0 gives the same work.
-    lse_ws.zero_()
     t_score = timed(f_score)
-    t_pass2 = timed(f_pass2)
     t_select = timed(f_select)
     t_compact = timed(f_compact)
+    t_pass2 = None
+    if args.pass_breakdown:
+        lse0 = torch.zeros((w.B, w.H, w.P), dtype=torch.float32, device=dev)  # same work as any finite LSE
+
+        def f_pass2(l):
+            q, k, v = data[l]
+            nacl.score(prob, q, k, ws, lse=lse0, out=outs[l][0])
+        t_pass2 = timed(f_pass2)
     step()  # restore the real outputs of every layer
     torch.cuda.synchronize()
+    status = int(ws[4:8].view(torch.int32).item())
+    if status:
+        raise RuntimeError("score kernel reported a wait that hit its spin limit")
     ab = alg_bytes(w)
     fl = alg_flops(w)
     peak_tf = F32_PEAK_TFLOPS if w.dtype == "f32" else BF16_PEAK_TFLOPS
-    t_pass1 = t_score - t_pass2
     stages = {
-        "score_pass1_combine_us": round(t_pass1, 2),
-        "score_pass2_us": round(t_pass2, 2),
         "score_us": round(t_score, 2),
         "select_us": round(t_select, 2),
         "compact_us": round(t_compact, 2),
         "layer_us": round(ms_per_step / layers * 1e3, 2),
         "score_alg_GBps": round(ab["score"] / (t_score * 1e3), 1),
-        "score_mfma_util_alg": round(fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
-        "score_mfma_util_exec": round(2 * fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
-        "pass2_mfma_util": round(fl / (t_pass2 * 1e-6) / (peak_tf * 1e12), 4),
+        "score_mfma_frac_alg": round(fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
+        "score_mfma_frac_exec": round(2 * fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
         "select_alg_GBps": round(ab["select"] / (t_select * 1e3), 1),
         "compact_alg_GBps": round(ab["compact"] / (t_compact * 1e3), 1),
+        "compact_hbm_frac": round(ab["compact"] / (t_compact * 1e3) / HBM_PEAK_GBS, 4),
         "select_compact_hbm_frac": round((ab["select"] + ab["compact"]) /
                                          ((t_select + t_compact) * 1e3) / HBM_PEAK_GBS, 4),
     }
+    if t_pass2 is not None:
+        stages["score_pass2_only_us"] = round(t_pass2, 2)
     log(f"[bench] stages {json.dumps(stages)}")
 
-    # Dominant single kernel: the longest of pass 2 and compaction (pass 1 +
-    # combine is two launches).
-    if t_compact >= t_pass2:
-        dom = {"kernel": "compact_kernel", "bound": "hbm", "us": t_compact,
-               "achieved": ab["compact"] / (t_compact * 1e3), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
-    else:
-        dom = {"kernel": "score_pass2_kernel", "bound": "hbm", "us": t_pass2,
-               "achieved": ab["score"] / (t_pass2 * 1e3), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    # Dominant kernel: score_kernel.  Its roofline is HBM (algorithmic
+    # intensity P flop/byte, below the bf16 ridge of ~312): algorithmic bytes
+    # = K read once + proxy rows of Q + F written, per launch (one layer).
+    dom = {"kernel": "score_kernel", "bound": "hbm", "us": t_score,
+           "achieved": ab["score"] / (t_score * 1e3), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     traffic = None
-    if MEASURED_TRAFFIC and MEASURED_TRAFFIC.get("kernel") == dom["kernel"] \
-            and MEASURED_TRAFFIC.get("workload") == w.name:
+    if MEASURED_TRAFFIC and MEASURED_TRAFFIC.get("workload") == w.name and \
+            MEASURED_TRAFFIC.get("source_sha") == _source_sha("paper_2408_03675_amd/csrc/score.hip"):
         traffic = MEASURED_TRAFFIC["bytes_per_launch"]
     roofline = {"bound": dom["bound"], "achieved": round(dom["achieved"], 1), "peak": dom["peak"],
                 "unit": dom["unit"], "frac": round(dom["achieved"] / dom["peak"], 4),
-                "traffic": traffic, "kernel": dom["kernel"], "avg_us": round(dom["us"], 2)}
+                "traffic": traffic, "kernel": dom["kernel"], "avg_us": round(dom["us"], 2),
+                "alg_bytes_per_launch": ab["score"]}
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, data[0], args.cpu_heads)
+        cpu = cpu_baseline(w, data, args.cpu_seconds)
         log(f"[bench] cpu baseline {json.dumps(cpu)}")
 
     line = {
@@ -216,29 +235,60 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(w, layer0, n_heads):
-    """The oracle, as it stands, on heads of batch row 0 of layer 0 (host
-    copies of the GPU inputs).  tokens/s = L * n_heads / H / t: the rate at
-    which it would evict one sequence's layer."""
-    import numpy as np
+def run_probe(which, w, prob, ws, layer0, out0):
+    """Three launches of one kernel on layer 0, nothing else timed: the
+    program rocprofv3 --pmc runs to read a kernel's HBM counters.  "copy" is
+    the calibration: a plain 1 GiB device-to-device copy (1 GiB read, 1 GiB
+    written per launch)."""
     import torch
+    from paper_2408_03675_amd import nacl
+    q, k, v = layer0
+    F, keep, ko, vo = out0
+    nacl.evict(prob, q, k, v, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, 0, ws=ws, scores=F,
+               keep_idx=keep, k_out=ko, v_out=vo)
+    torch.cuda.synchronize()
+    if which == "copy":
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=q.device)
+        src.fill_(1)
+        dst = torch.empty_like(src)
+    for _ in range(3):
+        if which == "score":
+            nacl.score(prob, q, k, ws, out=F)
+        elif which == "select":
+            nacl.select(prob, F, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, 0, ws=ws, out=keep)
+        elif which == "compact":
+            nacl.compact(prob, k, v, keep, k_out=ko, v_out=vo)
+        else:
+            dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] probe {which} done")
+
+
+def cpu_baseline(w, data, seconds):
+    """The oracle, as it stands, on whole layers of the same workload (host
+    copies of the GPU inputs), layer after layer until `seconds` have passed
+    (at least one layer).  tokens/s = B * L * layers done / time, the same
+    per-layer rate as the GPU figure."""
+    import numpy as np
     from threadpoolctl import threadpool_info
     from oracle import evict as o_evict
 
-    q, k, v = layer0
-    n_heads = min(n_heads, w.H)
-    qh = q[0:1, :n_heads].float().cpu().numpy()
-    kh = k[0:1, :n_heads].float().cpu().numpy()
-    vh = v[0:1, :n_heads].float().cpu().numpy()
-    t0 = time.perf_counter()
-    o_evict(qh, kh, vh, w.proxy_pos, w.n_protect, w.C, w.Cr, 0, w.rng_seed, 0, w.scale)
-    dt = time.perf_counter() - t0
+    done, spent = 0, 0.0
+    for l, (q, k, v) in enumerate(data):
+        qh, kh, vh = (t.float().cpu().numpy() for t in (q, k, v))
+        t0 = time.perf_counter()
+        o_evict(qh, kh, vh, w.proxy_pos, w.n_protect, w.C, w.Cr, 0, w.rng_seed, l, w.scale)
+        spent += time.perf_counter() - t0
+        done += 1
+        del qh, kh, vh
+        if spent >= seconds:
+            break
     blas = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
     threads = max(blas) if blas else 1
-    return {"value": round(w.L * n_heads / w.H / dt, 1), "unit": "tokens/s", "cores": int(threads),
+    return {"value": round(w.B * w.L * done / spent, 1), "unit": "tokens/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"layer 0, batch row 0, heads 0..{n_heads - 1} of {w.name} "
-                      f"({n_heads}/{w.B * w.H} of one layer's heads), float64 NumPy, {dt:.1f}s",
+            "sample": f"{done} whole layer(s) of {w.name} (all {w.B * w.H} heads each), float64 NumPy "
+                      f"oracle, {spent:.1f} s; BLAS on {threads} threads, elementwise work single-threaded",
             "host_cpus": len(os.sched_getaffinity(0))}
 
 

@@ -1,0 +1,113 @@
+"""The C ABI of libnacl.so on the host: the library loads, exports every
+entry point include/nacl.h declares, sizes workspaces, and rejects invalid
+arguments before touching the GPU (these calls never reach the HIP runtime,
+so they run without a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+nacl = pytest.importorskip("paper_2408_03675_amd.nacl")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(nacl.LIB_PATH):
+        pytest.skip("libnacl.so not built")
+    return nacl.load_library()
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "nacl.h")).read()
+    return sorted(set(re.findall(r"\b(nacl_[a-z_]+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert set(names) == set(nacl.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.nacl_version() == 1
+
+
+def _prob(**kw):
+    args = dict(B=2, H=4, L=1000, D=128, dtype="bf16", proxy_pos=list(range(900, 1000)))
+    args.update(kw)
+    return nacl.Problem(args["B"], args["H"], args["L"], args["D"], args["dtype"], args["proxy_pos"],
+                        n_protect=kw.get("n_protect"), sm_scale=kw.get("sm_scale"))
+
+
+def test_workspace_bytes(lib):
+    n1 = nacl.workspace_bytes(_prob())
+    n2 = nacl.workspace_bytes(_prob(L=2000, proxy_pos=list(range(1900, 2000))))
+    n3 = nacl.workspace_bytes(_prob(B=4))
+    assert 0 < n1 < n2 and n1 < n3
+    assert n1 % 256 == 0
+    assert nacl.workspace_bytes(_prob(D=96)) == 0
+
+
+FAKE = ctypes.c_void_p(1 << 20)  # never dereferenced: validation fails first
+
+
+def _status(lib, fn, *args):
+    return fn(*args)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(D=96), nacl.NACL_ERR_UNSUPPORTED),
+    (dict(proxy_pos=[5, 5, 6]), nacl.NACL_ERR_INVALID_ARG),
+    (dict(proxy_pos=[10, 3]), nacl.NACL_ERR_INVALID_ARG),
+    (dict(proxy_pos=[1000]), nacl.NACL_ERR_INVALID_ARG),
+    (dict(proxy_pos=[-1]), nacl.NACL_ERR_INVALID_ARG),
+    (dict(L=0, proxy_pos=[0]), nacl.NACL_ERR_INVALID_ARG),
+    (dict(n_protect=101), nacl.NACL_ERR_INVALID_ARG),
+    (dict(sm_scale=-1.0), nacl.NACL_ERR_INVALID_ARG),
+    (dict(L=(1 << 19) + 1, proxy_pos=[0]), nacl.NACL_ERR_UNSUPPORTED),
+])
+def test_problem_validation(lib, kw, code):
+    p = _prob(**kw)
+    st = lib.nacl_score(p.ref(), FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None)
+    assert st == code, lib.nacl_last_error_detail()
+    assert lib.nacl_last_error_detail()
+
+
+def test_score_argument_checks(lib):
+    p = _prob()
+    ws = nacl.workspace_bytes(p)
+    assert lib.nacl_score(p.ref(), None, FAKE, None, FAKE, FAKE, ws, None) == nacl.NACL_ERR_INVALID_ARG
+    assert lib.nacl_score(p.ref(), FAKE, FAKE, None, FAKE, FAKE, ws - 1, None) == nacl.NACL_ERR_WORKSPACE
+    assert lib.nacl_score(p.ref(), FAKE, FAKE, None, FAKE, None, ws, None) == nacl.NACL_ERR_WORKSPACE
+    misaligned = ctypes.c_void_p((1 << 20) + 8)
+    assert lib.nacl_score(p.ref(), FAKE, FAKE, None, FAKE, misaligned, ws, None) == nacl.NACL_ERR_WORKSPACE
+    assert lib.nacl_score(p.ref(), misaligned, FAKE, None, FAKE, FAKE, ws, None) == nacl.NACL_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("C,Cr,mode", [(1001, 10, 0), (-1, 0, 0), (150, -2, 0), (120, 30, 0), (400, 100, 3)])
+def test_select_argument_checks(lib, C, Cr, mode):
+    p = _prob()  # 100 protected proxies
+    ws = nacl.workspace_bytes(p)
+    st = lib.nacl_select(p.ref(), FAKE, C, Cr, mode, 0, 0, FAKE, FAKE, ws, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG, lib.nacl_last_error_detail()
+
+
+def test_compact_overlap_rejected(lib):
+    p = _prob()
+    k = (1 << 30)
+    kbytes = 2 * 4 * 1000 * 128 * 2
+    # k_out starting inside K
+    st = lib.nacl_compact(p.ref(), ctypes.c_void_p(k), ctypes.c_void_p(k + 2 * kbytes), ctypes.c_void_p(k + 8 * kbytes),
+                          200, ctypes.c_void_p(k + 4096), ctypes.c_void_p(k + 4 * kbytes), None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # k_out and v_out overlapping each other
+    st = lib.nacl_compact(p.ref(), ctypes.c_void_p(k), ctypes.c_void_p(k + 2 * kbytes), ctypes.c_void_p(k + 8 * kbytes),
+                          200, ctypes.c_void_p(k + 4 * kbytes), ctypes.c_void_p(k + 4 * kbytes + 256), None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+
+
+def test_status_strings(lib):
+    for code in range(5):
+        assert lib.nacl_status_string(code)
+    assert lib.nacl_status_string(99) == b"unknown status"
