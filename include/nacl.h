@@ -96,7 +96,12 @@ size_t nacl_workspace_bytes(const nacl_problem* p);
  * as a FlashAttention-2 forward returns it (Appendix A.7, Algorithm 2); with
  * it only the column reduction runs.  NULL: the library computes it (two
  * passes over K).  scores: device fp32 [B,H,L], fully overwritten; keys after
- * the last proxy get 0. */
+ * the last proxy get 0.
+ * Health word: once the stream has completed the call, the 32-bit word at
+ * byte offset 4 of the workspace is 0.  Bit 0 set means a wave of the
+ * two-pass kernel gave up waiting for a head's log-sum-exp after its bounded
+ * spin (never expected; the scores of that call are then not valid).  The
+ * next nacl_score or nacl_evict call on the workspace clears it. */
 int nacl_score(const nacl_problem* p, const void* q, const void* k, const float* lse,
                float* scores, void* ws, size_t ws_bytes, void* stream);
 
