@@ -26,9 +26,14 @@ namespace nacl {
 #define NACL_SCORE_GROUP_ITEMS_PER_CU 2
 #endif
 #ifndef NACL_SCORE_LAG
-#define NACL_SCORE_LAG 2
+#define NACL_SCORE_LAG 1
+#endif
+// LDS ring per key group for streamed K tiles (bytes).
+#ifndef NACL_SCORE_RING_BYTES
+#define NACL_SCORE_RING_BYTES 16384
 #endif
 constexpr int kScoreTilesPerWave = NACL_SCORE_TPW;
+constexpr int kScoreRingBytes = NACL_SCORE_RING_BYTES;
 constexpr int kScoreWavesPerSimd = NACL_SCORE_WAVES;
 constexpr int kScoreKeyGroups = NACL_SCORE_KEY_GROUPS;
 constexpr int kScoreChunkKeys = kScoreTilesPerWave * kScoreKeyGroups * 16;

@@ -125,9 +125,10 @@ struct KStage {
   static constexpr int kInstr = 16 / kRowsPerInstr;  // DMA instructions per tile
   static constexpr int kTileBytes = 16 * kRowBytes;
   static constexpr int kSwz = (kChunks < 8 ? kChunks : 8) - 1;
-  // Ring depth: 16 KB of LDS per wave at 4 KB tiles, at least double
-  // buffering, at most 4 (one __shared__ array per slot, see score_kernel).
-  static constexpr int kDepth = kTileBytes >= 8192 ? 2 : 4;
+  // Ring depth in tiles (one __shared__ array per slot, see score_kernel):
+  // kScoreRingBytes of LDS per key group, at least double buffering, at most 8.
+  static constexpr int kDepth =
+      kScoreRingBytes / kTileBytes < 2 ? 2 : (kScoreRingBytes / kTileBytes > 8 ? 8 : kScoreRingBytes / kTileBytes);
 
   // Lane byte offsets inside a tile, one per DMA instruction.
   __device__ static void offsets(uint32_t row_bytes, int lane, uint32_t (&vo)[kInstr]) {
@@ -220,14 +221,61 @@ __device__ __forceinline__ ItemRef decode_item(const ScoreSched& s, int i) {
 }
 
 // Pass 1 over one tile of 16 keys: folds the tile's logits into the running
-// base-2 (max, sum) of the 16*PB proxies (m in raw logit units).  FULL: every
-// key of the tile is visible to every proxy of the group (no mask).  Proxy
-// blocks go in batches of kHalf so at most kHalf accumulators are live.
-template <typename M, int PB, bool FULL>
-__device__ __forceinline__ void pass1_tile(const typename M::frag_t (&kf)[M::kSteps],
-                                           const typename M::frag_t (&qf)[PB][M::kSteps], int key0,
-                                           const int* pos_g, int g, int r16, float c2, float (&m)[PB],
-                                           float (&sm)[PB]) {
+// base-2 (max, sum) of the 16*PB proxies (m in raw logit units, the sum
+// relative to exp2(m * c2)).  Proxy blocks go in batches of kHalf so at most
+// kHalf accumulators are live.
+//
+// Tiles where every key is visible to every proxy of the group (the common
+// case) keep the reference max lazily: terms may exceed exp2(m * c2) by up to
+// 2^kLazyLog2, and only a tile whose max passes that threshold in some lane
+// rescales, on a wave-uniform branch.  Tiles that straddle a proxy position
+// mask keys past each proxy and update the max exactly.
+constexpr float kLazyLog2 = 8.f;
+
+template <typename M, int PB>
+__device__ __forceinline__ void pass1_tile_full(const typename M::frag_t (&kf)[M::kSteps],
+                                                const typename M::frag_t (&qf)[PB][M::kSteps], float c2,
+                                                float lazy_raw, float (&m)[PB], float (&sm)[PB]) {
+  constexpr int kHalf = PB > 4 ? 4 : PB;
+#pragma unroll
+  for (int p0 = 0; p0 < PB; p0 += kHalf) {
+    f32x4 acc[kHalf];
+#pragma unroll
+    for (int j = 0; j < kHalf; ++j) {
+      acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < M::kSteps; ++ks) acc[j] = M::mma(kf[ks], qf[p0 + j][ks], acc[j]);
+    }
+    bool over = false;
+#pragma unroll
+    for (int j = 0; j < kHalf; ++j)
+      over |= fmaxf(fmaxf(fmaxf(acc[j][0], acc[j][1]), acc[j][2]), acc[j][3]) > m[p0 + j] + lazy_raw;
+    if (__builtin_amdgcn_ballot_w64(over)) {
+#pragma unroll
+      for (int j = 0; j < kHalf; ++j) {
+        const int pb = p0 + j;
+        const float mx = fmaxf(fmaxf(fmaxf(acc[j][0], acc[j][1]), acc[j][2]), acc[j][3]);
+        const float mn = fmaxf(m[pb], mx);
+        sm[pb] = (m[pb] == -INFINITY) ? 0.f : sm[pb] * fast_exp2((m[pb] - mn) * c2);
+        m[pb] = mn;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kHalf; ++j) {
+      const int pb = p0 + j;
+      const float mc = m[pb] * c2;
+      float sum = fast_exp2(fmaf(acc[j][0], c2, -mc)) + fast_exp2(fmaf(acc[j][1], c2, -mc));
+      sum += fast_exp2(fmaf(acc[j][2], c2, -mc)) + fast_exp2(fmaf(acc[j][3], c2, -mc));
+      sm[pb] += sum;
+    }
+  }
+}
+
+template <typename M, int PB>
+__device__ __forceinline__ void pass1_tile_masked(const typename M::frag_t (&kf)[M::kSteps],
+                                                  const typename M::frag_t (&qf)[PB][M::kSteps], int key0,
+                                                  const int* pos_g, int g, int r16, float c2, float (&m)[PB],
+                                                  float (&sm)[PB]) {
   constexpr int kHalf = PB > 4 ? 4 : PB;
 #pragma unroll
   for (int p0 = 0; p0 < PB; p0 += kHalf) {
@@ -242,31 +290,20 @@ __device__ __forceinline__ void pass1_tile(const typename M::frag_t (&kf)[M::kSt
     for (int j = 0; j < kHalf; ++j) {
       const int pb = p0 + j;
       const f32x4 acc = acc_h[j];
-      if constexpr (FULL) {
-        const float mx = fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3]));
-        const float mn = fmaxf(m[pb], mx);
-        const float sc = fast_exp2((m[pb] - mn) * c2);
+      const int pi = pos_g[16 * pb + r16];
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = (key0 + 4 * g + e <= pi) ? acc[e] : -INFINITY;
+      const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+      const float mn = fmaxf(m[pb], mx);
+      if (mn != -INFINITY) {
+        const float sc = (m[pb] == -INFINITY) ? 0.f : fast_exp2((m[pb] - mn) * c2);
         const float mc = mn * c2;
-        float sum = fast_exp2(fmaf(acc[0], c2, -mc)) + fast_exp2(fmaf(acc[1], c2, -mc));
-        sum += fast_exp2(fmaf(acc[2], c2, -mc)) + fast_exp2(fmaf(acc[3], c2, -mc));
+        float sum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sum += (v[e] == -INFINITY) ? 0.f : fast_exp2(fmaf(v[e], c2, -mc));
         sm[pb] = fmaf(sm[pb], sc, sum);
         m[pb] = mn;
-      } else {
-        const int pi = pos_g[16 * pb + r16];
-        float v[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = (key0 + 4 * g + e <= pi) ? acc[e] : -INFINITY;
-        const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        const float mn = fmaxf(m[pb], mx);
-        if (mn != -INFINITY) {
-          const float sc = (m[pb] == -INFINITY) ? 0.f : fast_exp2((m[pb] - mn) * c2);
-          const float mc = mn * c2;
-          float sum = 0.f;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) sum += (v[e] == -INFINITY) ? 0.f : fast_exp2(fmaf(v[e], c2, -mc));
-          sm[pb] = fmaf(sm[pb], sc, sum);
-          m[pb] = mn;
-        }
       }
     }
   }
@@ -306,6 +343,19 @@ __device__ __forceinline__ float pass2_tile(const typename M::frag_t (&kf)[M::kS
   return cs;
 }
 
+// Column sums of four consecutive tiles: x[t] holds, in lane (g, r16), the
+// sum over lane group g's proxy rows for key r16 of tile t.  Two
+// v_permlane32_swap and one v_permlane16_swap transpose the four lane groups
+// so that lane group g returns the full column sum of tile g.
+__device__ __forceinline__ float colsum4(float x0, float x1, float x2, float x3) {
+  auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0), __float_as_uint(x2), false, false);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x1), __float_as_uint(x3), false, false);
+  const float y0 = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const float y1 = __uint_as_float(b[0]) + __uint_as_float(b[1]);
+  auto c = __builtin_amdgcn_permlane16_swap(__float_as_uint(y0), __float_as_uint(y1), false, false);
+  return __uint_as_float(c[0]) + __uint_as_float(c[1]);
+}
+
 // Work-group layout: kScoreKeyGroups key groups x 2 proxy halves, one wave
 // each.  The two waves of a key group share one LDS ring of K tiles and each
 // holds the Q fragments of half of the proxy group, which keeps registers low
@@ -325,21 +375,23 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
   constexpr int kDmaPerWave = KS::kInstr / 2;
   static_assert(PB % 2 == 0, "proxy groups split over two waves");
   static_assert(KS::kInstr % 2 == 0, "tile DMA split over two waves");
-  static_assert(TPW % KS::kDepth == 0, "tiles per key group vs ring depth");
+  constexpr int kUnroll = KS::kDepth > 4 ? KS::kDepth : 4;  // tiles per unrolled step
+  static_assert(kUnroll % KS::kDepth == 0 && TPW % kUnroll == 0, "tiles per key group vs ring depth");
   constexpr int NK = kScoreKeyGroups;
   static_assert(NK * kKeysPerPair == kScoreChunkKeys, "item size");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kGroup];
   __shared__ float2 red[NK][kGroup];
+  __shared__ float2 mrg[kScoreThreads];
   __shared__ float col_lds[2 * NK][kKeysPerPair];
   __shared__ __attribute__((aligned(16))) float lse_g[kGroup];
   // One array per ring slot: distinct objects let the compiler see that a
   // DMA into one slot does not alias reads of another, so it does not wait
   // for outstanding DMA before every LDS read.
-  __shared__ __attribute__((aligned(16))) unsigned char kslot0[NK][KS::kTileBytes];
-  __shared__ __attribute__((aligned(16))) unsigned char kslot1[NK][KS::kTileBytes];
-  __shared__ __attribute__((aligned(16))) unsigned char kslot2[NK][KS::kDepth > 2 ? KS::kTileBytes : 16];
-  __shared__ __attribute__((aligned(16))) unsigned char kslot3[NK][KS::kDepth > 2 ? KS::kTileBytes : 16];
+#define NACL_KSLOT(i) \
+  __shared__ __attribute__((aligned(16))) unsigned char kslot##i[NK][KS::kDepth > i ? KS::kTileBytes : 16];
+  NACL_KSLOT(0) NACL_KSLOT(1) NACL_KSLOT(2) NACL_KSLOT(3) NACL_KSLOT(4) NACL_KSLOT(5) NACL_KSLOT(6) NACL_KSLOT(7)
+#undef NACL_KSLOT
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -367,7 +419,11 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       if constexpr (u == 0) return kslot0[kp];
       else if constexpr (u == 1) return kslot1[kp];
       else if constexpr (u == 2) return kslot2[kp];
-      else return kslot3[kp];
+      else if constexpr (u == 3) return kslot3[kp];
+      else if constexpr (u == 4) return kslot4[kp];
+      else if constexpr (u == 5) return kslot5[kp];
+      else if constexpr (u == 6) return kslot6[kp];
+      else return kslot7[kp];
     };
     // Runs step(t, tile) over the key group's TPW tiles.  Tiles stream
     // through the pair's LDS ring of kDepth slots: tile t + kDepth - 1 is in
@@ -390,17 +446,18 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         if (u < TPW) issue_tile(u, slot(u_c));
       });
 #pragma unroll 1
-      for (int t = 0; t < TPW; t += KS::kDepth) {
-        static_for<KS::kDepth>([&](auto u_c) {
+      for (int t = 0; t < TPW; t += kUnroll) {
+        static_for<kUnroll>([&](auto u_c) {
           constexpr int u = decltype(u_c)::value;
           const int tt = t + u;
           wait_dma_tiles<kDmaPerWave, KS::kDepth - 2>(min(KS::kDepth - 2, TPW - 1 - tt));
           __syncthreads();
           typename M::frag_t kf[kS];
-          M::template from_lds<KS::kChunks, KS::kSwz>(slot(u_c), r16, g, kf);
+          M::template from_lds<KS::kChunks, KS::kSwz>(slot(std::integral_constant<int, u % KS::kDepth>{}), r16, g,
+                                                      kf);
           const int tn = tt + KS::kDepth - 1;
           if (tn < TPW) issue_tile(tn, slot(std::integral_constant<int, (u + KS::kDepth - 1) % KS::kDepth>{}));
-          step(tt, kf);
+          step(tt, kf, u_c);
         });
       }
     };
@@ -439,10 +496,11 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
           m[pb] = -INFINITY;
           sm[pb] = 0.f;
         }
-        auto step1 = [&](int t, const typename M::frag_t (&kf)[kS]) {
+        const float lazy_raw = kLazyLog2 / c2;
+        auto step1 = [&](int t, const typename M::frag_t (&kf)[kS], auto) {
           const int key0 = key_base + t * 16;
-          if (key0 + 15 <= first) pass1_tile<M, PBW, true>(kf, qf, key0, my_pos, g, r16, c2, m, sm);
-          else if (key0 <= last) pass1_tile<M, PBW, false>(kf, qf, key0, my_pos, g, r16, c2, m, sm);
+          if (key0 + 15 <= first) pass1_tile_full<M, PBW>(kf, qf, c2, lazy_raw, m, sm);
+          else if (key0 <= last) pass1_tile_masked<M, PBW>(kf, qf, key0, my_pos, g, r16, c2, m, sm);
         };
         k_stream(step1);
         // Merge the four lane groups (different keys, same proxy), then the key groups.
@@ -467,14 +525,38 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       if (threadIdx.x == 0) last_s = atomicAdd(&s.head_cnt[bh], 1u) == (unsigned)(s.n_chunks - 1);
       __syncthreads();
       if (last_s) {
+        // Merge the head's n_chunks partials per proxy: `split` threads share
+        // a proxy, each taking every split-th chunk with kBatch loads in
+        // flight, and combine through LDS.
         const float2* hp = s.partials + (int64_t)bh * s.n_chunks * a.P;
-        for (int i = threadIdx.x; i < a.P; i += kScoreThreads) {
+        const int split = a.P >= kScoreThreads ? 1 : kScoreThreads / a.P;
+        const int part = threadIdx.x / a.P;  // >= split for idle threads when P does not divide
+        constexpr int kBatch = 8;
+        for (int i0 = 0; i0 < a.P; i0 += kScoreThreads) {
+          const int i = i0 + (split == 1 ? (int)threadIdx.x : (int)threadIdx.x % a.P);
           float mm = -INFINITY, ss = 0.f;
-          for (int c = 0; c < s.n_chunks; ++c) {
-            const float2 v = load_coherent(hp + (int64_t)c * a.P + i);
-            lse_merge(mm, ss, v.x, v.y);
+          if (i < a.P && part < split) {
+            for (int c0 = part; c0 < s.n_chunks; c0 += kBatch * split) {
+              float2 v[kBatch];
+#pragma unroll
+              for (int u = 0; u < kBatch; ++u) {
+                const int c = c0 + u * split;
+                v[u] = c < s.n_chunks ? load_coherent(hp + (int64_t)c * a.P + i) : make_float2(-INFINITY, 0.f);
+              }
+#pragma unroll
+              for (int u = 0; u < kBatch; ++u) lse_merge(mm, ss, v[u].x, v[u].y);
+            }
           }
-          store_coherent(s.lse2 + (int64_t)bh * a.P + i, mm + __log2f(ss));
+          if (split > 1) {
+            mrg[threadIdx.x] = make_float2(mm, ss);
+            __syncthreads();
+            if (part == 0 && i < a.P)
+              for (int pp = 1; pp < split; ++pp) {
+                const float2 r = mrg[threadIdx.x + pp * a.P];
+                lse_merge(mm, ss, r.x, r.y);
+              }
+          }
+          if (part == 0 && i < a.P) store_coherent(s.lse2 + (int64_t)bh * a.P + i, mm + __log2f(ss));
         }
         wait_stores();
         __syncthreads();
@@ -513,14 +595,22 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         const float* my_lse = lse_g + ph * kHalfRows;
         // Column sums over this wave's proxies, accumulated across proxy
         // groups in the wave's own LDS row (same-wave LDS accesses are ordered).
-        auto step2 = [&](int t, const typename M::frag_t (&kf)[kS]) {
+        // This lane's partial column sums of the last four tiles; every
+        // fourth tile they are reduced across lane groups and lane group g
+        // stores tile t - 3 + g.
+        float cs4[4];
+        auto step2 = [&](int t, const typename M::frag_t (&kf)[kS], auto u_c) {
+          constexpr int u = decltype(u_c)::value;
           const int key0 = key_base + t * 16;
           float cs = 0.f;
           if (key0 + 15 <= first) cs = pass2_tile<M, PBW, true>(kf, qf, key0, my_pos, g, r16, c2, my_lse);
           else if (key0 <= last) cs = pass2_tile<M, PBW, false>(kf, qf, key0, my_pos, g, r16, c2, my_lse);
-          cs += __shfl_xor(cs, 16);
-          cs += __shfl_xor(cs, 32);
-          if (g == 0) my_cols[t * 16 + r16] = (g0 == 0 ? 0.f : my_cols[t * 16 + r16]) + cs;
+          cs4[u % 4] = cs;
+          if constexpr (u % 4 == 3) {
+            const float z = colsum4(cs4[0], cs4[1], cs4[2], cs4[3]);
+            const int idx = (t - 3) * 16 + lane;
+            my_cols[idx] = (g0 == 0 ? 0.f : my_cols[idx]) + z;
+          }
         };
         k_stream(step2);
       }
