@@ -15,7 +15,7 @@ namespace nacl {
 #define NACL_SCORE_TPW 32
 #endif
 #ifndef NACL_SCORE_WAVES
-#define NACL_SCORE_WAVES 3
+#define NACL_SCORE_WAVES 2
 #endif
 #ifndef NACL_SCORE_KEY_GROUPS
 #define NACL_SCORE_KEY_GROUPS 2
