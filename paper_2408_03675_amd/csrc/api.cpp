@@ -45,7 +45,7 @@ constexpr int kCounterHeader = 64;  // queue + status words, padded to 256 bytes
 Layout layout_of(const nacl_problem* p) {
   Layout l;
   const size_t BH = (size_t)p->B * p->H;
-  l.n_chunks = (p->L + nacl::kScoreChunkKeys - 1) / nacl::kScoreChunkKeys;
+  l.n_chunks = (p->L + nacl::kScoreMinChunkKeys - 1) / nacl::kScoreMinChunkKeys;  // most chunks any call uses
   size_t off = 0;
   l.cnt = off;
   off += align_up((kCounterHeader + BH) * sizeof(uint32_t));
@@ -184,12 +184,23 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
     return fail(NACL_ERR_HIP, "querying the device");
   const int BH = p->B * p->H;
   nacl::ScoreSched& sc = s.sched;
-  sc.n_chunks = l.n_chunks;
-  sc.heads_per_group = heads_per_group(BH, l.n_chunks, NACL_SCORE_GROUP_ITEMS_PER_CU * cus);
+  sc.lse_given = lse != nullptr;
+  // Item size: the largest tpw whose items still number at least four per
+  // resident work-group (two per CU); long items amortise the per-item Q
+  // loads, partial stores and pipeline fill, too few leave a long tail.
+  const int passes = sc.lse_given ? 1 : 2;
+  sc.tpw = nacl::kScoreTpwMin;
+  for (int t = nacl::kScoreTpwMin * 2; t <= nacl::kScoreTpwMax; t *= 2) {
+    const int ck = t * nacl::kScoreKeyGroups * 16;
+    const int64_t items = (int64_t)passes * BH * ((p->L + ck - 1) / ck);
+    if (items >= 4 * 2 * (int64_t)cus) sc.tpw = t;
+  }
+  sc.chunk_keys = sc.tpw * nacl::kScoreKeyGroups * 16;
+  sc.n_chunks = (p->L + sc.chunk_keys - 1) / sc.chunk_keys;  // <= l.n_chunks
+  sc.heads_per_group = heads_per_group(BH, sc.n_chunks, NACL_SCORE_GROUP_ITEMS_PER_CU * cus);
   sc.n_groups = BH / sc.heads_per_group;
   sc.lag = std::min(NACL_SCORE_LAG, sc.n_groups);
-  sc.lse_given = lse != nullptr;
-  sc.total_items = (sc.lse_given ? 1 : 2) * BH * l.n_chunks;
+  sc.total_items = passes * BH * sc.n_chunks;
   uint32_t* words = reinterpret_cast<uint32_t*>(ws + l.cnt);
   sc.queue = words;
   sc.status = words + 1;

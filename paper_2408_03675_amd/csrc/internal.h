@@ -8,11 +8,11 @@
 
 namespace nacl {
 
-// Score kernel shape.  A work item spans 2 key groups x kScoreTilesPerWave
+// Score kernel shape.  A work item spans 2 key groups x tpw
 // tiles of 16 keys; kScoreWavesPerSimd is the occupancy the register
 // allocation targets.
-#ifndef NACL_SCORE_TPW
-#define NACL_SCORE_TPW 32
+#ifndef NACL_SCORE_TPW_MAX
+#define NACL_SCORE_TPW_MAX 128
 #endif
 #ifndef NACL_SCORE_WAVES
 #define NACL_SCORE_WAVES 2
@@ -32,11 +32,14 @@ namespace nacl {
 #ifndef NACL_SCORE_RING_BYTES
 #define NACL_SCORE_RING_BYTES 16384
 #endif
-constexpr int kScoreTilesPerWave = NACL_SCORE_TPW;
+// Tiles per key group and item: chosen per call among kScoreTpwMin * 2^i up
+// to kScoreTpwMax.  The workspace is sized for the smallest.
+constexpr int kScoreTpwMin = 32;
+constexpr int kScoreTpwMax = NACL_SCORE_TPW_MAX;
 constexpr int kScoreRingBytes = NACL_SCORE_RING_BYTES;
 constexpr int kScoreWavesPerSimd = NACL_SCORE_WAVES;
 constexpr int kScoreKeyGroups = NACL_SCORE_KEY_GROUPS;
-constexpr int kScoreChunkKeys = kScoreTilesPerWave * kScoreKeyGroups * 16;
+constexpr int kScoreMinChunkKeys = kScoreTpwMin * kScoreKeyGroups * 16;
 
 struct ScoreArgs {
   int B, H, L, P;
@@ -48,7 +51,9 @@ struct ScoreArgs {
 
 // Work queue of the persistent score kernel (see score.hip).
 struct ScoreSched {
-  int n_chunks;          // key chunks per head (kScoreChunkKeys keys each)
+  int tpw;               // tiles of 16 keys per key group and item (multiple of 4)
+  int chunk_keys;        // keys per item: kScoreKeyGroups * tpw * 16
+  int n_chunks;          // key chunks per head
   int heads_per_group;   // heads per scheduling group
   int n_groups;          // B*H / heads_per_group
   int lag;               // pass-2 items of group g follow pass-1 items of group g + lag

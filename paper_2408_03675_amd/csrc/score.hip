@@ -4,7 +4,7 @@
 // causal keys 0..p_i.
 //
 // One persistent kernel runs two kinds of work items over key chunks of
-// kScoreChunkKeys keys, all on MFMA (v_mfma_f32_16x16x32_bf16 for bf16
+// sched.chunk_keys keys, all on MFMA (v_mfma_f32_16x16x32_bf16 for bf16
 // inputs, v_mfma_f32_16x16x4_f32 for fp32 inputs):
 //   pass 1  online base-2 (max, sum) of every proxy row over the chunk's keys
 //           -> per-chunk partials; the last chunk of a head to finish merges
@@ -359,9 +359,9 @@ __device__ __forceinline__ float colsum4(float x0, float x1, float x2, float x3)
 // Work-group layout: kScoreKeyGroups key groups x 2 proxy halves, one wave
 // each.  The two waves of a key group share one LDS ring of K tiles and each
 // holds the Q fragments of half of the proxy group, which keeps registers low
-// enough for three waves per SIMD.  Each key group covers TPW consecutive
-// tiles, so an item spans kScoreKeyGroups * TPW * 16 keys.
-template <typename T, int D, int PB, int TPW>
+// enough for two waves per SIMD.  Each key group covers s.tpw consecutive
+// tiles (at most TPWMAX), so an item spans kScoreKeyGroups * s.tpw * 16 keys.
+template <typename T, int D, int PB, int TPWMAX>
 __global__ __launch_bounds__(kScoreThreads)
 __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) void score_kernel(
     const T* __restrict__ q, const T* __restrict__ k, ScoreArgs a, ScoreSched s) {
@@ -371,19 +371,18 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
   constexpr int kGroup = 16 * PB;        // proxies per group
   constexpr int PBW = PB / 2;            // proxy blocks per wave
   constexpr int kHalfRows = 16 * PBW;    // proxies per wave
-  constexpr int kKeysPerPair = TPW * 16;
+  constexpr int kMaxKeysPerPair = TPWMAX * 16;
   constexpr int kDmaPerWave = KS::kInstr / 2;
   static_assert(PB % 2 == 0, "proxy groups split over two waves");
   static_assert(KS::kInstr % 2 == 0, "tile DMA split over two waves");
   constexpr int kUnroll = KS::kDepth > 4 ? KS::kDepth : 4;  // tiles per unrolled step
-  static_assert(kUnroll % KS::kDepth == 0 && TPW % kUnroll == 0, "tiles per key group vs ring depth");
+  static_assert(kUnroll % KS::kDepth == 0 && kScoreTpwMin % kUnroll == 0, "tiles per key group vs ring depth");
   constexpr int NK = kScoreKeyGroups;
-  static_assert(NK * kKeysPerPair == kScoreChunkKeys, "item size");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kGroup];
   __shared__ float2 red[NK][kGroup];
   __shared__ float2 mrg[kScoreThreads];
-  __shared__ float col_lds[2 * NK][kKeysPerPair];
+  __shared__ float col_lds[2 * NK][kMaxKeysPerPair];
   __shared__ __attribute__((aligned(16))) float lse_g[kGroup];
   // One array per ring slot: distinct objects let the compiler see that a
   // DMA into one slot does not alias reads of another, so it does not wait
@@ -410,7 +409,9 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     const int bh = it.bh, b = bh / a.H, h = bh % a.H;
     const T* qb = q + b * a.qs[0] + h * a.qs[1];
     const T* kb = k + b * a.ks[0] + h * a.ks[1];
-    const int chunk_key0 = it.chunk * kScoreChunkKeys;
+    const int TPW = s.tpw;  // multiple of kUnroll, at most TPWMAX
+    const int kKeysPerPair = TPW * 16;
+    const int chunk_key0 = it.chunk * s.chunk_keys;
     const int key_base = chunk_key0 + kp * kKeysPerPair;
     const bool beyond = chunk_key0 > a.p_last;  // no proxy sees these keys
 
@@ -564,7 +565,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       }
     } else if (beyond) {
       float* F = s.scores + (int64_t)bh * a.L;
-      const int end = min(chunk_key0 + kScoreChunkKeys, a.L);
+      const int end = min(chunk_key0 + s.chunk_keys, a.L);
       for (int j = chunk_key0 + threadIdx.x; j < end; j += kScoreThreads) F[j] = 0.f;
     } else {
       // ---------------- pass 2: column sums of exp2(logit - LSE) ----------
@@ -616,7 +617,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       }
       __syncthreads();
       float* F = s.scores + (int64_t)bh * a.L;
-      for (int idx = threadIdx.x; idx < kScoreChunkKeys; idx += kScoreThreads) {
+      for (int idx = threadIdx.x; idx < s.chunk_keys; idx += kScoreThreads) {
         const int pair = idx / kKeysPerPair, j = idx % kKeysPerPair;
         const int key = chunk_key0 + idx;
         if (key < a.L) F[key] = col_lds[2 * pair][j] + col_lds[2 * pair + 1][j];
@@ -637,7 +638,7 @@ namespace {
 
 template <typename T, int D, int PB>
 hipError_t launch_score_t(const ScoreLaunch& L, hipStream_t stream) {
-  auto kern = score_kernel<T, D, PB, kScoreTilesPerWave>;
+  auto kern = score_kernel<T, D, PB, kScoreTpwMax>;
   int per_cu = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kScoreThreads, 0);
   if (e != hipSuccess) return e;
