@@ -109,6 +109,14 @@ template <int D> struct Mma<float, D> {
   }
 };
 
+// Cache policy of the K tile loads: 2 = nt (streaming).  Each pass reads K
+// once; on a plain LDS-DMA ring the streaming hint raised the rate from 5.6
+// to 6.2 TB/s (the score kernel itself times the same either way).
+#ifndef NACL_SCORE_DMA_AUX
+#define NACL_SCORE_DMA_AUX 2
+#endif
+constexpr int kScoreDmaAux = NACL_SCORE_DMA_AUX;
+
 // A 16-key tile of K staged in LDS by direct buffer->LDS loads
 // (buffer_load_dwordx4 ... lds: each lane moves 16 bytes, and one
 // instruction fills 1 KB of LDS in lane order).  Row r of the tile occupies
@@ -146,7 +154,7 @@ struct KStage {
     for (int j = 0; j < kInstr / 2; ++j) {
       const int i = 2 * j + half;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(dst + i * 1024),
-                                               16, vo[i], tile_byte, 0, 0);
+                                               16, vo[i], tile_byte, 0, kScoreDmaAux);
     }
   }
 };
