@@ -191,11 +191,11 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   const int passes = sc.lse_given ? 1 : 2;
   sc.tpw = nacl::kScoreTpwMin;
   for (int t = nacl::kScoreTpwMin * 2; t <= nacl::kScoreTpwMax; t *= 2) {
-    const int ck = t * nacl::kScoreKeyGroups * 16;
+    const int ck = t * nacl::kScoreWaves * 16;
     const int64_t items = (int64_t)passes * BH * ((p->L + ck - 1) / ck);
     if (items >= 4 * 2 * (int64_t)cus) sc.tpw = t;
   }
-  sc.chunk_keys = sc.tpw * nacl::kScoreKeyGroups * 16;
+  sc.chunk_keys = sc.tpw * nacl::kScoreWaves * 16;
   sc.n_chunks = (p->L + sc.chunk_keys - 1) / sc.chunk_keys;  // <= l.n_chunks
   sc.heads_per_group = heads_per_group(BH, sc.n_chunks, NACL_SCORE_GROUP_ITEMS_PER_CU * cus);
   sc.n_groups = BH / sc.heads_per_group;

@@ -8,17 +8,13 @@
 
 namespace nacl {
 
-// Score kernel shape.  A work item spans 2 key groups x tpw
-// tiles of 16 keys; kScoreWavesPerSimd is the occupancy the register
-// allocation targets.
+// Score kernel shape.  A work item spans kScoreWaves waves x tpw tiles of 16
+// keys; kScoreWavesPerSimd is the occupancy the register allocation targets.
 #ifndef NACL_SCORE_TPW_MAX
-#define NACL_SCORE_TPW_MAX 128
+#define NACL_SCORE_TPW_MAX 32
 #endif
 #ifndef NACL_SCORE_WAVES
 #define NACL_SCORE_WAVES 2
-#endif
-#ifndef NACL_SCORE_KEY_GROUPS
-#define NACL_SCORE_KEY_GROUPS 2
 #endif
 // Scheduling: pass-1 items of about GROUP_ITEMS_PER_CU * CUs items form a
 // head group; pass-2 items of group g follow pass-1 items of group g + LAG.
@@ -28,18 +24,13 @@ namespace nacl {
 #ifndef NACL_SCORE_LAG
 #define NACL_SCORE_LAG 1
 #endif
-// LDS ring per key group for streamed K tiles (bytes).
-#ifndef NACL_SCORE_RING_BYTES
-#define NACL_SCORE_RING_BYTES 16384
-#endif
-// Tiles per key group and item: chosen per call among kScoreTpwMin * 2^i up
-// to kScoreTpwMax.  The workspace is sized for the smallest.
+// Tiles per wave and item: chosen per call among kScoreTpwMin * 2^i up to
+// kScoreTpwMax.  The workspace is sized for the smallest.
 constexpr int kScoreTpwMin = 32;
 constexpr int kScoreTpwMax = NACL_SCORE_TPW_MAX;
-constexpr int kScoreRingBytes = NACL_SCORE_RING_BYTES;
 constexpr int kScoreWavesPerSimd = NACL_SCORE_WAVES;
-constexpr int kScoreKeyGroups = NACL_SCORE_KEY_GROUPS;
-constexpr int kScoreMinChunkKeys = kScoreTpwMin * kScoreKeyGroups * 16;
+constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter of the item's keys
+constexpr int kScoreMinChunkKeys = kScoreTpwMin * kScoreWaves * 16;
 
 struct ScoreArgs {
   int B, H, L, P;
@@ -51,8 +42,8 @@ struct ScoreArgs {
 
 // Work queue of the persistent score kernel (see score.hip).
 struct ScoreSched {
-  int tpw;               // tiles of 16 keys per key group and item (multiple of 4)
-  int chunk_keys;        // keys per item: kScoreKeyGroups * tpw * 16
+  int tpw;               // tiles of 16 keys per wave and item (multiple of 4)
+  int chunk_keys;        // keys per item: kScoreWaves * tpw * 16
   int n_chunks;          // key chunks per head
   int heads_per_group;   // heads per scheduling group
   int n_groups;          // B*H / heads_per_group

@@ -6,35 +6,45 @@
 // One persistent kernel runs two kinds of work items over key chunks of
 // sched.chunk_keys keys, all on MFMA (v_mfma_f32_16x16x32_bf16 for bf16
 // inputs, v_mfma_f32_16x16x4_f32 for fp32 inputs):
-//   pass 1  online base-2 (max, sum) of every proxy row over the chunk's keys
+//   pass 1  base-2 (reference, sum) of every proxy row over the chunk's keys
 //           -> per-chunk partials; the last chunk of a head to finish merges
 //           the head's partials into its log-sum-exp
 //   pass 2  exp2(logit - LSE) summed over the proxy rows for each key of the
 //           chunk -> F (the column reduction of Appendix A.7's Algorithm 2).
-//           Each key tile is owned by one wave: no atomics on F, so results
-//           are bit-reproducible.
+//           Each key is owned by one wave: no atomics on F, so results are
+//           bit-reproducible.
+//
+// The kernel streams K straight from HBM into registers: each wave owns a
+// contiguous quarter of the chunk's keys and all proxies of the current proxy
+// group, so a K tile is used by exactly one wave and never staged in LDS.
+// Tiles of 16 keys are fetched with 16-byte non-temporal buffer loads a few
+// tiles ahead of the MFMAs that consume them (a register ring), which streams
+// at close to the HBM rate.  Pass 2 reads K a second time; a memory-side cache
+// does not serve that re-read faster than HBM on this part, so K crosses HBM
+// twice and the kernel is bound by 2 x |K| / HBM bandwidth.
 //
 // Work-groups take items from a queue counter in a fixed order: the pass-1
-// items of head group g + lag come before the pass-2 items of head group g.
-// A pass-2 item therefore re-reads keys that pass 1 streamed from HBM shortly
-// before, which the 256 MB memory-side Infinity Cache still holds, so K
-// crosses HBM about once.  A pass-2 item waits (bounded spin) until its
-// head's log-sum-exp is published; every item it waits on was taken from the
-// queue earlier by a running work-group and never waits itself, so the wait
-// always ends, whatever the number of resident work-groups.
+// items of head group g + lag come before the pass-2 items of head group g,
+// so a pass-2 item rarely finds its head's log-sum-exp unpublished.  A
+// pass-2 item waits (bounded spin) until its head's log-sum-exp is published;
+// every item it waits on was taken from the queue earlier by a running
+// work-group and never waits itself, so the wait always ends, whatever the
+// number of resident work-groups.
 //
 // Fragment layout.  A 16x16 MFMA tile is indexed by (lane % 16) along M/N and
-// by the lane group g = lane / 16 along the contraction.  Lane group g holds
-// the contiguous d-slice [g*D/4, (g+1)*D/4) of its row, for Q and K alike;
-// contraction step s uses elements [s*E, (s+1)*E) of that slice (E = 8 for
-// bf16, 1 for fp32).  Any permutation of the contraction index is harmless as
-// long as both operands use the same one, and this one lets every lane fetch
-// its slice with 16-byte loads.  The 16x16 accumulator holds rows
-// 4*g + e (e = 0..3) and column lane % 16.
+// by the lane group g = lane / 16 along the contraction.  The head dimension
+// is cut into 64-byte pieces; piece c of a row holds d in [c*P, (c+1)*P)
+// (P = 32 bf16 or 16 fp32 elements) and lane group g takes its 16-byte part
+// [c*P + g*P/4, c*P + (g+1)*P/4).  For bf16 piece c is contraction step c (a
+// 16x16x32 step consumes 8 elements per lane); for fp32 element i of the
+// lane's part is step 4c + i (a 16x16x4 step consumes one).  Q and K use the
+// same map, so the permutation of the contraction index cancels, and one
+// 16-byte load instruction reads 64 contiguous bytes of each of 16 rows.  The
+// 16x16 accumulator holds rows 4*g + e (e = 0..3) and column lane % 16.
 //   pass 1 computes K_tile * Q_P^T: rows = keys, columns = proxies, so each
-//          lane keeps running statistics for one proxy.
+//          lane keeps the running statistics of one proxy per block.
 //   pass 2 computes Q_P * K_tile^T: rows = proxies, columns = keys, so each
-//          lane sums one key's column in registers and two cross-lane adds
+//          lane sums one key's column in registers and cross-lane moves
 //          finish it.
 
 #include <type_traits>
@@ -44,15 +54,33 @@
 
 namespace nacl {
 
+// Cache policy of the K tile loads: 2 = nt (streaming).  Each pass reads K
+// once per proxy group and nothing re-reads it soon after.
+#ifndef NACL_SCORE_K_AUX
+#define NACL_SCORE_K_AUX 2
+#endif
+constexpr int kScoreKAux = NACL_SCORE_K_AUX;
+
+// Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data format).
+constexpr int kBufferRsrcWord3 = 0x00020000;
+// A byte offset beyond every descriptor's range (num_records < 2^31) that
+// cannot wrap when a lane offset below 2^30 is added.
+constexpr uint32_t kOutOfRange = 0xC0000000u;
+
 template <typename T, int D> struct Mma;
+
+// Proxy blocks whose accumulators are live at once.
+#ifndef NACL_SCORE_HALF
+#define NACL_SCORE_HALF 4
+#endif
 
 template <int D> struct Mma<__bf16, D> {
   static constexpr int kSteps = D / 32;
   typedef bf16x8 frag_t;
   __device__ static void load(const __bf16* row, int g, frag_t (&f)[kSteps]) {
-    const u32x4* p = reinterpret_cast<const u32x4*>(row + g * (D / 4));
+    const u32x4* p = reinterpret_cast<const u32x4*>(row + 8 * g);
 #pragma unroll
-    for (int s = 0; s < kSteps; ++s) f[s] = __builtin_bit_cast(frag_t, p[s]);
+    for (int s = 0; s < kSteps; ++s) f[s] = __builtin_bit_cast(frag_t, p[4 * s]);
   }
   __device__ static void zero(frag_t (&f)[kSteps]) {
 #pragma unroll
@@ -61,15 +89,13 @@ template <int D> struct Mma<__bf16, D> {
   __device__ static f32x4 mma(frag_t a, frag_t b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
-  // Fragment of row r16 from a staged K tile (see KStage); one 16-byte chunk
-  // per contraction step.
-  template <int kChunks, int kSwz>
-  __device__ static void from_lds(const unsigned char* tile, int r16, int g, frag_t (&f)[kSteps]) {
+  // This lane's fragment of one K row read directly through the head's
+  // buffer descriptor at byte offset off (the whole offset is range-checked:
+  // rows past the descriptor's end read as zeros).  Used by the exact path.
+  __device__ static void load_k(__amdgpu_buffer_rsrc_t r, uint32_t off, frag_t (&f)[kSteps]) {
 #pragma unroll
-    for (int s = 0; s < kSteps; ++s) {
-      const int x = (g * kSteps + s) ^ (r16 & kSwz);
-      f[s] = __builtin_bit_cast(frag_t, *reinterpret_cast<const u32x4*>(tile + (r16 * kChunks + x) * 16));
-    }
+    for (int s = 0; s < kSteps; ++s)
+      f[s] = __builtin_bit_cast(frag_t, __builtin_amdgcn_raw_buffer_load_b128(r, off + 64u * s, 0, kScoreKAux));
   }
 };
 
@@ -77,10 +103,10 @@ template <int D> struct Mma<float, D> {
   static constexpr int kSteps = D / 4;
   typedef float frag_t;
   __device__ static void load(const float* row, int g, frag_t (&f)[kSteps]) {
-    const float4* p = reinterpret_cast<const float4*>(row + g * (D / 4));
+    const float4* p = reinterpret_cast<const float4*>(row + 4 * g);
 #pragma unroll
     for (int s = 0; s < kSteps / 4; ++s) {
-      const float4 v = p[s];
+      const float4 v = p[4 * s];
       f[4 * s + 0] = v.x;
       f[4 * s + 1] = v.y;
       f[4 * s + 2] = v.z;
@@ -94,37 +120,26 @@ template <int D> struct Mma<float, D> {
   __device__ static f32x4 mma(frag_t a, frag_t b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
   }
-  // Four contraction steps per 16-byte chunk.
-  template <int kChunks, int kSwz>
-  __device__ static void from_lds(const unsigned char* tile, int r16, int g, frag_t (&f)[kSteps]) {
+  __device__ static void load_k(__amdgpu_buffer_rsrc_t r, uint32_t off, frag_t (&f)[kSteps]) {
 #pragma unroll
-    for (int cc = 0; cc < kSteps / 4; ++cc) {
-      const int x = (g * (kSteps / 4) + cc) ^ (r16 & kSwz);
-      const f32x4 v = *reinterpret_cast<const f32x4*>(tile + (r16 * kChunks + x) * 16);
-      f[4 * cc + 0] = v[0];
-      f[4 * cc + 1] = v[1];
-      f[4 * cc + 2] = v[2];
-      f[4 * cc + 3] = v[3];
+    for (int c = 0; c < kSteps / 4; ++c) {
+      const f32x4 v = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off + 64u * c, 0, kScoreKAux));
+      f[4 * c + 0] = v[0];
+      f[4 * c + 1] = v[1];
+      f[4 * c + 2] = v[2];
+      f[4 * c + 3] = v[3];
     }
   }
 };
 
-// Cache policy of the K tile loads: 2 = nt (streaming).  Each pass reads K
-// once; on a plain LDS-DMA ring the streaming hint raised the rate from 5.6
-// to 6.2 TB/s (the score kernel itself times the same either way).
-#ifndef NACL_SCORE_DMA_AUX
-#define NACL_SCORE_DMA_AUX 2
-#endif
-constexpr int kScoreDmaAux = NACL_SCORE_DMA_AUX;
-
-// A 16-key tile of K staged in LDS by direct buffer->LDS loads
-// (buffer_load_dwordx4 ... lds: each lane moves 16 bytes, and one
-// instruction fills 1 KB of LDS in lane order).  Row r of the tile occupies
+// One wave's 16-key tile of K staged in LDS by direct buffer->LDS loads
+// (buffer_load_dwordx4 ... lds: each lane moves 16 bytes and one instruction
+// fills 1 KB of LDS in lane order).  An instruction reads kRowsPerInstr whole
+// rows, so its global accesses are contiguous.  Row r of the tile occupies
 // kChunks consecutive 16-byte slots; slot x holds the row's chunk
-// x ^ (r & kSwz), an XOR swizzle that spreads the fragment reads of 16 rows
-// over the LDS banks.  Addressing goes through a buffer descriptor of the
-// head's K rows: rows at or past L fall outside it and read as zeros (their
-// keys are masked), and the tile position is a scalar offset.
+// x ^ (r & kSwz), an XOR swizzle under which the 16 rows of a fragment read
+// fall on distinct LDS banks.  Offsets go through the head's buffer
+// descriptor (whole offset range-checked: rows at or past L read as zeros).
 template <typename T, int D>
 struct KStage {
   static constexpr int kRowBytes = D * (int)sizeof(T);
@@ -132,11 +147,10 @@ struct KStage {
   static constexpr int kRowsPerInstr = 64 / kChunks;
   static constexpr int kInstr = 16 / kRowsPerInstr;  // DMA instructions per tile
   static constexpr int kTileBytes = 16 * kRowBytes;
-  static constexpr int kSwz = (kChunks < 8 ? kChunks : 8) - 1;
-  // Ring depth in tiles (one __shared__ array per slot, see score_kernel):
-  // kScoreRingBytes of LDS per key group, at least double buffering, at most 8.
-  static constexpr int kDepth =
-      kScoreRingBytes / kTileBytes < 2 ? 2 : (kScoreRingBytes / kTileBytes > 8 ? 8 : kScoreRingBytes / kTileBytes);
+  static constexpr int kSwz = (kChunks < 16 ? kChunks : 16) - 1;
+  // Ring depth per wave: 16 KB of tiles (two work-groups share a CU's LDS),
+  // at least 2 and at most 8.
+  static constexpr int kDepth = 16384 / kTileBytes < 2 ? 2 : (16384 / kTileBytes > 8 ? 8 : 16384 / kTileBytes);
 
   // Lane byte offsets inside a tile, one per DMA instruction.
   __device__ static void offsets(uint32_t row_bytes, int lane, uint32_t (&vo)[kInstr]) {
@@ -147,14 +161,32 @@ struct KStage {
       vo[i] = (uint32_t)row * row_bytes + (uint32_t)c * 16u;
     }
   }
-  // The DMA instructions i = half, half + 2, ... of one tile.
-  __device__ static void issue_half(__amdgpu_buffer_rsrc_t rsrc, const uint32_t (&vo)[kInstr],
-                                    uint32_t tile_byte, unsigned char* dst, int half) {
+  __device__ static void issue(__amdgpu_buffer_rsrc_t rsrc, const uint32_t (&vo)[kInstr], uint32_t tile_byte,
+                               unsigned char* dst) {
 #pragma unroll
-    for (int j = 0; j < kInstr / 2; ++j) {
-      const int i = 2 * j + half;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(dst + i * 1024),
-                                               16, vo[i], tile_byte, 0, kScoreDmaAux);
+    for (int i = 0; i < kInstr; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(dst + i * 1024), 16,
+                                               vo[i] + tile_byte, 0, 0, kScoreKAux);
+  }
+  // Fragment of row r16 (lane group g): 16-byte chunk 4*c + g of piece c.
+  template <typename M>
+  __device__ static void frag(const unsigned char* tile, int r16, int g, typename M::frag_t (&f)[M::kSteps]) {
+    if constexpr (std::is_same_v<T, __bf16>) {
+#pragma unroll
+      for (int c = 0; c < M::kSteps; ++c) {
+        const int x = (4 * c + g) ^ (r16 & kSwz);
+        f[c] = __builtin_bit_cast(typename M::frag_t, *reinterpret_cast<const u32x4*>(tile + (r16 * kChunks + x) * 16));
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < M::kSteps / 4; ++c) {
+        const int x = (4 * c + g) ^ (r16 & kSwz);
+        const f32x4 v = *reinterpret_cast<const f32x4*>(tile + (r16 * kChunks + x) * 16);
+        f[4 * c + 0] = v[0];
+        f[4 * c + 1] = v[1];
+        f[4 * c + 2] = v[2];
+        f[4 * c + 3] = v[3];
+      }
     }
   }
 };
@@ -173,9 +205,7 @@ __device__ __forceinline__ void wait_dma_tiles(int remaining) {
   }
 }
 
-constexpr int kScoreThreads = 128 * kScoreKeyGroups;  // 2 waves per key group
-// Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data format).
-constexpr int kBufferRsrcWord3 = 0x00020000;
+constexpr int kScoreThreads = 64 * kScoreWaves;
 
 // Calls f(std::integral_constant<int, i>) for i = 0 .. N-1.
 template <int N, int I = 0, class F>
@@ -228,127 +258,19 @@ __device__ __forceinline__ ItemRef decode_item(const ScoreSched& s, int i) {
   return ItemRef{kind, group * s.heads_per_group + r / s.n_chunks, r % s.n_chunks};
 }
 
-// Pass 1 over one tile of 16 keys: folds the tile's logits into the running
-// base-2 (max, sum) of the 16*PB proxies (m in raw logit units, the sum
-// relative to exp2(m * c2)).  Proxy blocks go in batches of kHalf so at most
-// kHalf accumulators are live.
-//
-// Tiles where every key is visible to every proxy of the group (the common
-// case) keep the reference max lazily: terms may exceed exp2(m * c2) by up to
-// 2^kLazyLog2, and only a tile whose max passes that threshold in some lane
-// rescales, on a wave-uniform branch.  Tiles that straddle a proxy position
-// mask keys past each proxy and update the max exactly.
-constexpr float kLazyLog2 = 8.f;
-
-template <typename M, int PB>
-__device__ __forceinline__ void pass1_tile_full(const typename M::frag_t (&kf)[M::kSteps],
-                                                const typename M::frag_t (&qf)[PB][M::kSteps], float c2,
-                                                float lazy_raw, float (&m)[PB], float (&sm)[PB]) {
-  constexpr int kHalf = PB > 4 ? 4 : PB;
+// Logits of one 16-key tile for proxy blocks [P0, P0 + N) into acc[0 .. N):
+// pass-1 orientation (rows = keys) when KROWS, pass-2 orientation (rows =
+// proxies) otherwise.
+template <typename M, int PB, int P0, int N, bool KROWS, int NA>
+__device__ __forceinline__ void tile_logits(const typename M::frag_t (&kf)[M::kSteps],
+                                            const typename M::frag_t (&qf)[PB][M::kSteps], f32x4 (&acc)[NA]) {
 #pragma unroll
-  for (int p0 = 0; p0 < PB; p0 += kHalf) {
-    f32x4 acc[kHalf];
+  for (int j = 0; j < N; ++j) {
+    acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < kHalf; ++j) {
-      acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < M::kSteps; ++ks) acc[j] = M::mma(kf[ks], qf[p0 + j][ks], acc[j]);
-    }
-    bool over = false;
-#pragma unroll
-    for (int j = 0; j < kHalf; ++j)
-      over |= fmaxf(fmaxf(fmaxf(acc[j][0], acc[j][1]), acc[j][2]), acc[j][3]) > m[p0 + j] + lazy_raw;
-    if (__builtin_amdgcn_ballot_w64(over)) {
-#pragma unroll
-      for (int j = 0; j < kHalf; ++j) {
-        const int pb = p0 + j;
-        const float mx = fmaxf(fmaxf(fmaxf(acc[j][0], acc[j][1]), acc[j][2]), acc[j][3]);
-        const float mn = fmaxf(m[pb], mx);
-        sm[pb] = (m[pb] == -INFINITY) ? 0.f : sm[pb] * fast_exp2((m[pb] - mn) * c2);
-        m[pb] = mn;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kHalf; ++j) {
-      const int pb = p0 + j;
-      const float mc = m[pb] * c2;
-      float sum = fast_exp2(fmaf(acc[j][0], c2, -mc)) + fast_exp2(fmaf(acc[j][1], c2, -mc));
-      sum += fast_exp2(fmaf(acc[j][2], c2, -mc)) + fast_exp2(fmaf(acc[j][3], c2, -mc));
-      sm[pb] += sum;
-    }
+    for (int ks = 0; ks < M::kSteps; ++ks)
+      acc[j] = KROWS ? M::mma(kf[ks], qf[P0 + j][ks], acc[j]) : M::mma(qf[P0 + j][ks], kf[ks], acc[j]);
   }
-}
-
-template <typename M, int PB>
-__device__ __forceinline__ void pass1_tile_masked(const typename M::frag_t (&kf)[M::kSteps],
-                                                  const typename M::frag_t (&qf)[PB][M::kSteps], int key0,
-                                                  const int* pos_g, int g, int r16, float c2, float (&m)[PB],
-                                                  float (&sm)[PB]) {
-  constexpr int kHalf = PB > 4 ? 4 : PB;
-#pragma unroll
-  for (int p0 = 0; p0 < PB; p0 += kHalf) {
-    f32x4 acc_h[kHalf];
-#pragma unroll
-    for (int j = 0; j < kHalf; ++j) {
-      acc_h[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < M::kSteps; ++ks) acc_h[j] = M::mma(kf[ks], qf[p0 + j][ks], acc_h[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < kHalf; ++j) {
-      const int pb = p0 + j;
-      const f32x4 acc = acc_h[j];
-      const int pi = pos_g[16 * pb + r16];
-      float v[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = (key0 + 4 * g + e <= pi) ? acc[e] : -INFINITY;
-      const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-      const float mn = fmaxf(m[pb], mx);
-      if (mn != -INFINITY) {
-        const float sc = (m[pb] == -INFINITY) ? 0.f : fast_exp2((m[pb] - mn) * c2);
-        const float mc = mn * c2;
-        float sum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sum += (v[e] == -INFINITY) ? 0.f : fast_exp2(fmaf(v[e], c2, -mc));
-        sm[pb] = fmaf(sm[pb], sc, sum);
-        m[pb] = mn;
-      }
-    }
-  }
-}
-
-// Pass 2 over one tile of 16 keys: this lane's share of its key's column sum
-// of exp2(logit - LSE) over the 16*PB proxies (lse_g: base-2 LSE per row).
-template <typename M, int PB, bool FULL>
-__device__ __forceinline__ float pass2_tile(const typename M::frag_t (&kf)[M::kSteps],
-                                            const typename M::frag_t (&qf)[PB][M::kSteps], int key0,
-                                            const int* pos_g, int g, int r16, float c2,
-                                            const float* lse_g) {
-  // Proxy blocks in batches of kHalf so at most kHalf accumulators are live.
-  constexpr int kHalf = PB > 4 ? 4 : PB;
-  float cs = 0.f;
-#pragma unroll
-  for (int p0 = 0; p0 < PB; p0 += kHalf) {
-    f32x4 acc[kHalf];
-#pragma unroll
-    for (int j = 0; j < kHalf; ++j) {
-      acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < M::kSteps; ++ks) acc[j] = M::mma(qf[p0 + j][ks], kf[ks], acc[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < kHalf; ++j) {
-      const int pb = p0 + j;
-      const f32x4 lr = *reinterpret_cast<const f32x4*>(lse_g + 16 * pb + 4 * g);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float x = fast_exp2(fmaf(acc[j][e], c2, -lr[e]));
-        if constexpr (FULL) cs += x;
-        else cs += (key0 + r16 <= pos_g[16 * pb + 4 * g + e]) ? x : 0.f;
-      }
-    }
-  }
-  return cs;
 }
 
 // Column sums of four consecutive tiles: x[t] holds, in lane (g, r16), the
@@ -364,48 +286,64 @@ __device__ __forceinline__ float colsum4(float x0, float x1, float x2, float x3)
   return __uint_as_float(c[0]) + __uint_as_float(c[1]);
 }
 
-// Work-group layout: kScoreKeyGroups key groups x 2 proxy halves, one wave
-// each.  The two waves of a key group share one LDS ring of K tiles and each
-// holds the Q fragments of half of the proxy group, which keeps registers low
-// enough for two waves per SIMD.  Each key group covers s.tpw consecutive
-// tiles (at most TPWMAX), so an item spans kScoreKeyGroups * s.tpw * 16 keys.
+// An integer the compiler cannot see through: LDS reads indexed with it are
+// re-issued where they stand instead of being hoisted out of the tile loop
+// into (scarce) registers.
+__device__ __forceinline__ int opaque(int x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// Maximum over the 4 lane groups (same r16) of a per-lane value.
+__device__ __forceinline__ float max_over_groups(float x) {
+  x = fmaxf(x, __shfl_xor(x, 16));
+  return fmaxf(x, __shfl_xor(x, 32));
+}
+__device__ __forceinline__ float sum_over_groups(float x) {
+  x += __shfl_xor(x, 16);
+  return x + __shfl_xor(x, 32);
+}
+
+// Work-group layout: kScoreWaves waves, each owning s.tpw consecutive tiles
+// of 16 keys (at most TPWMAX) and the Q fragments of the whole proxy group of
+// 16*PB proxies.  An item spans kScoreWaves * s.tpw * 16 keys.
 template <typename T, int D, int PB, int TPWMAX>
 __global__ __launch_bounds__(kScoreThreads)
 __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) void score_kernel(
     const T* __restrict__ q, const T* __restrict__ k, ScoreArgs a, ScoreSched s) {
   using M = Mma<T, D>;
-  using KS = KStage<T, D>;
+  using frag_t = typename M::frag_t;
   constexpr int kS = M::kSteps;
   constexpr int kGroup = 16 * PB;        // proxies per group
-  constexpr int PBW = PB / 2;            // proxy blocks per wave
-  constexpr int kHalfRows = 16 * PBW;    // proxies per wave
-  constexpr int kMaxKeysPerPair = TPWMAX * 16;
-  constexpr int kDmaPerWave = KS::kInstr / 2;
-  static_assert(PB % 2 == 0, "proxy groups split over two waves");
-  static_assert(KS::kInstr % 2 == 0, "tile DMA split over two waves");
-  constexpr int kUnroll = KS::kDepth > 4 ? KS::kDepth : 4;  // tiles per unrolled step
-  static_assert(kUnroll % KS::kDepth == 0 && kScoreTpwMin % kUnroll == 0, "tiles per key group vs ring depth");
-  constexpr int NK = kScoreKeyGroups;
+  constexpr int kMaxKeysPerWave = TPWMAX * 16;
+  constexpr int kHalf = PB > NACL_SCORE_HALF ? NACL_SCORE_HALF : PB;  // live accumulators (exact path)
+  constexpr int kUnroll = KStage<T, D>::kDepth > 4 ? KStage<T, D>::kDepth : 4;  // tiles per unrolled step
+  static_assert(kUnroll % KStage<T, D>::kDepth == 0 && kScoreTpwMin % kUnroll == 0, "tiles per wave vs ring");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kGroup];
-  __shared__ float2 red[NK][kGroup];
+  __shared__ float2 red[kScoreWaves][kGroup];
   __shared__ float2 mrg[kScoreThreads];
-  __shared__ float col_lds[2 * NK][kMaxKeysPerPair];
+  __shared__ float col_lds[kScoreWaves][kMaxKeysPerWave];
   __shared__ __attribute__((aligned(16))) float lse_g[kGroup];
+  using KS = KStage<T, D>;
+  constexpr int kDepth = KS::kDepth;
   // One array per ring slot: distinct objects let the compiler see that a
   // DMA into one slot does not alias reads of another, so it does not wait
   // for outstanding DMA before every LDS read.
 #define NACL_KSLOT(i) \
-  __shared__ __attribute__((aligned(16))) unsigned char kslot##i[NK][KS::kDepth > i ? KS::kTileBytes : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char kslot##i[kScoreWaves][kDepth > i ? KS::kTileBytes : 16];
   NACL_KSLOT(0) NACL_KSLOT(1) NACL_KSLOT(2) NACL_KSLOT(3) NACL_KSLOT(4) NACL_KSLOT(5) NACL_KSLOT(6) NACL_KSLOT(7)
 #undef NACL_KSLOT
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int kp = wave >> 1, ph = wave & 1;  // key group, proxy half
   const int r16 = lane & 15, g = lane >> 4;
   const float c2 = a.c2;
   float* my_cols = col_lds[wave];
+  const uint32_t row_bytes = (uint32_t)(a.ks[2] * (int64_t)sizeof(T));
+  uint32_t vo[KStage<T, D>::kInstr];
+  KStage<T, D>::offsets(row_bytes, lane, vo);
+  const uint32_t voff = (uint32_t)r16 * row_bytes + 16u * (uint32_t)g;  // direct fragment loads (exact path)
 
   for (;;) {
     __syncthreads();
@@ -418,57 +356,57 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     const T* qb = q + b * a.qs[0] + h * a.qs[1];
     const T* kb = k + b * a.ks[0] + h * a.ks[1];
     const int TPW = s.tpw;  // multiple of kUnroll, at most TPWMAX
-    const int kKeysPerPair = TPW * 16;
+    const int keys_per_wave = TPW * 16;
     const int chunk_key0 = it.chunk * s.chunk_keys;
-    const int key_base = chunk_key0 + kp * kKeysPerPair;
+    const int key_base = chunk_key0 + wave * keys_per_wave;
     const bool beyond = chunk_key0 > a.p_last;  // no proxy sees these keys
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + (uint32_t)(D * sizeof(T))),
+        kBufferRsrcWord3);
 
-    auto slot = [&](auto u_c) -> unsigned char* {
-      constexpr int u = decltype(u_c)::value;
-      if constexpr (u == 0) return kslot0[kp];
-      else if constexpr (u == 1) return kslot1[kp];
-      else if constexpr (u == 2) return kslot2[kp];
-      else if constexpr (u == 3) return kslot3[kp];
-      else if constexpr (u == 4) return kslot4[kp];
-      else if constexpr (u == 5) return kslot5[kp];
-      else if constexpr (u == 6) return kslot6[kp];
-      else return kslot7[kp];
+    // Streams the wave's TPW tiles through its own LDS ring of kDepth slots:
+    // tile t + kDepth - 1 is in flight while tile t is used.  Proxy blocks go
+    // in batches of kHalf (MFMAs, then their VALU work) so at most kHalf
+    // accumulators are live; the other wave on the SIMD fills the MFMA and
+    // VALU gaps.  Only this wave touches its ring, so no barrier is involved.
+    // The DMA is unconditional (a tile past the wave's range gets an offset
+    // beyond the descriptor and reads zeros without touching memory), so
+    // every wait count is static.
+    auto tile_byte = [&](int t) -> uint32_t {
+      return t < TPW ? (uint32_t)(key_base + 16 * t) * row_bytes : kOutOfRange;
     };
-    // Runs step(t, tile) over the key group's TPW tiles.  Tiles stream
-    // through the pair's LDS ring of kDepth slots: tile t + kDepth - 1 is in
-    // flight while tile t is read into registers and computed.  Each wave of
-    // the pair issues half of a tile's DMA and waits for its own half; the
-    // barrier then publishes the whole tile (and retires every read of the
-    // slot the next DMA overwrites).
-    auto k_stream = [&](auto&& step) {
-      const uint32_t row_bytes = (uint32_t)(a.ks[2] * (int64_t)sizeof(T));
-      const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<T*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + KS::kRowBytes),
-          kBufferRsrcWord3);
-      uint32_t vo[KS::kInstr];
-      KS::offsets(row_bytes, lane, vo);
-      auto issue_tile = [&](int t, unsigned char* dst) {
-        KS::issue_half(rsrc, vo, (uint32_t)(key_base + 16 * t) * row_bytes, dst, ph);
-      };
-      static_for<KS::kDepth - 1>([&](auto u_c) {
-        constexpr int u = decltype(u_c)::value;
-        if (u < TPW) issue_tile(u, slot(u_c));
-      });
+    auto slot = [&](auto u_c) -> unsigned char* {
+      constexpr int u = decltype(u_c)::value % kDepth;
+      if constexpr (u == 0) return kslot0[wave];
+      else if constexpr (u == 1) return kslot1[wave];
+      else if constexpr (u == 2) return kslot2[wave];
+      else if constexpr (u == 3) return kslot3[wave];
+      else if constexpr (u == 4) return kslot4[wave];
+      else if constexpr (u == 5) return kslot5[wave];
+      else if constexpr (u == 6) return kslot6[wave];
+      else return kslot7[wave];
+    };
+    auto k_stream = [&](auto&& mfma, auto&& valu) {
+      f32x4 acc[kHalf];
+      static_for<kDepth - 1>([&](auto u_c) { KS::issue(rsrc, vo, tile_byte(decltype(u_c)::value), slot(u_c)); });
 #pragma unroll 1
       for (int t = 0; t < TPW; t += kUnroll) {
         static_for<kUnroll>([&](auto u_c) {
           constexpr int u = decltype(u_c)::value;
           const int tt = t + u;
-          wait_dma_tiles<kDmaPerWave, KS::kDepth - 2>(min(KS::kDepth - 2, TPW - 1 - tt));
-          __syncthreads();
-          typename M::frag_t kf[kS];
-          M::template from_lds<KS::kChunks, KS::kSwz>(slot(std::integral_constant<int, u % KS::kDepth>{}), r16, g,
-                                                      kf);
-          const int tn = tt + KS::kDepth - 1;
-          if (tn < TPW) issue_tile(tn, slot(std::integral_constant<int, (u + KS::kDepth - 1) % KS::kDepth>{}));
-          step(tt, kf, u_c);
+          asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KS::kInstr * (kDepth - 2)) : "memory");
+          frag_t kf[kS];
+          KS::template frag<M>(slot(u_c), r16, g, kf);
+          KS::issue(rsrc, vo, tile_byte(tt + kDepth - 1), slot(std::integral_constant<int, u + kDepth - 1>{}));
+          static_for<PB / kHalf>([&](auto h_c) {
+            using P0 = std::integral_constant<int, decltype(h_c)::value * kHalf>;
+            using N = std::integral_constant<int, kHalf>;
+            mfma(tt, kf, acc, P0{}, N{});
+            valu(tt, acc, u_c, P0{}, N{});
+          });
         });
       }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     };
     // Positions of the proxy group [g0, g0 + gn), -1 past its end.
     auto load_group = [&](int g0, int gn) {
@@ -476,19 +414,18 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       for (int i = threadIdx.x; i < kGroup; i += kScoreThreads) pos_g[i] = i < gn ? a.pos[g0 + i] : -1;
       __syncthreads();
     };
-    // This wave's Q fragments: proxies kHalfRows * ph + [0, kHalfRows) of the group.
-    auto load_q = [&](int gn, typename M::frag_t (&qf)[PBW][kS]) {
+    // The Q fragments of the whole group (zeros past its end).
+    auto load_q = [&](int gn, frag_t (&qf)[PB][kS]) {
 #pragma unroll
-      for (int pb = 0; pb < PBW; ++pb) {
-        const int i = ph * kHalfRows + 16 * pb + r16;
+      for (int pb = 0; pb < PB; ++pb) {
+        const int i = 16 * pb + r16;
         if (i < gn) M::load(qb + (int64_t)pos_g[i] * a.qs[2], g, qf[pb]);
         else M::zero(qf[pb]);
       }
     };
-    const int* my_pos = pos_g + ph * kHalfRows;
 
     if (it.kind == 1) {
-      // ---------------- pass 1: per-chunk (max, sum) of every proxy row ----
+      // ---------------- pass 1: per-chunk (reference, sum) of every proxy row
       float2* part = s.partials + ((int64_t)bh * s.n_chunks + it.chunk) * a.P;
       if (beyond)
         for (int i = threadIdx.x; i < a.P; i += kScoreThreads)
@@ -497,34 +434,121 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         const int gn = min(kGroup, a.P - g0);
         load_group(g0, gn);
         const int first = pos_g[0], last = pos_g[gn - 1];
-        typename M::frag_t qf[PBW][kS];
+        frag_t qf[PB][kS];
         load_q(gn, qf);
-        float m[PBW], sm[PBW];
+        // Per proxy block: base-2 reference (the scaled maximum of the wave's
+        // first tile, 0 if that tile shows the proxy nothing) and the running
+        // sum of exp2(logit * c2 - ref) over this lane's keys.  Visibility is a
+        // prefix of the keys, so a proxy that sees nothing of the first tile
+        // sees nothing of the wave's keys; one that sees something has a sum of
+        // at least 1 (its reference key contributes exp2(0)).
+        float ref[PB], sm[PB];
 #pragma unroll
-        for (int pb = 0; pb < PBW; ++pb) {
-          m[pb] = -INFINITY;
+        for (int pb = 0; pb < PB; ++pb) {
+          ref[pb] = 0.f;
           sm[pb] = 0.f;
         }
-        const float lazy_raw = kLazyLog2 / c2;
-        auto step1 = [&](int t, const typename M::frag_t (&kf)[kS], auto) {
-          const int key0 = key_base + t * 16;
-          if (key0 + 15 <= first) pass1_tile_full<M, PBW>(kf, qf, c2, lazy_raw, m, sm);
-          else if (key0 <= last) pass1_tile_masked<M, PBW>(kf, qf, key0, my_pos, g, r16, c2, m, sm);
+        auto mfma1 = [&](int t, const frag_t (&kf)[kS], auto& acc, auto p0_c, auto n_c) {
+          if (key_base + t * 16 > last) return;  // no proxy of the group sees this tile
+          tile_logits<M, PB, decltype(p0_c)::value, decltype(n_c)::value, true>(kf, qf, acc);
         };
-        k_stream(step1);
-        // Merge the four lane groups (different keys, same proxy), then the key groups.
+        // VALU work of one tile; FULL tiles (every key visible to every proxy
+        // of the group, the common case) carry no masking at all.
+        auto valu1_body = [&](int t, const auto& acc, auto p0_c, auto n_c, auto full_c) {
+          constexpr int P0 = decltype(p0_c)::value, N = decltype(n_c)::value;
+          constexpr bool FULL = decltype(full_c)::value;
+          const int key0 = key_base + t * 16;
+          const int* pos_l = pos_g + opaque(r16);
 #pragma unroll
-        for (int pb = 0; pb < PBW; ++pb) {
-          float mm = m[pb] * c2, ss = sm[pb];
-          lse_merge(mm, ss, __shfl_xor(mm, 16), __shfl_xor(ss, 16));
-          lse_merge(mm, ss, __shfl_xor(mm, 32), __shfl_xor(ss, 32));
-          if (g == 0) red[kp][ph * kHalfRows + 16 * pb + r16] = make_float2(mm, ss);
+          for (int pb = P0; pb < P0 + N; ++pb) {
+            bool vis[4];
+            if constexpr (!FULL) {
+              const int pi = pos_l[16 * pb];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) vis[e] = key0 + 4 * g + e <= pi;
+            }
+            if (t == 0) {
+              float mx = -INFINITY;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) mx = (FULL || vis[e]) ? fmaxf(mx, acc[pb - P0][e]) : mx;
+              mx = max_over_groups(mx);
+              ref[pb] = mx != -INFINITY ? mx * c2 : 0.f;
+            }
+            float x[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb - P0][e], c2, -ref[pb]));
+            if constexpr (!FULL) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = vis[e] ? x[e] : 0.f;
+            }
+            sm[pb] += (x[0] + x[1]) + (x[2] + x[3]);
+          }
+        };
+        auto valu1 = [&](int t, const auto& acc, auto, auto p0_c, auto n_c) {
+          const int key0 = key_base + t * 16;
+          if (key0 > last) return;
+          if (key0 + 15 <= first) valu1_body(t, acc, p0_c, n_c, std::true_type{});
+          else valu1_body(t, acc, p0_c, n_c, std::false_type{});
+        };
+        k_stream(mfma1, valu1);
+        // Row sums over the four lane groups; a sum that overflowed (a key far
+        // above the first tile's maximum) is recomputed with the exact maximum.
+        bool bad = false;
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          sm[pb] = sum_over_groups(sm[pb]);
+          bad |= !(sm[pb] <= 3.0e38f);
+        }
+        if (__builtin_amdgcn_ballot_w64(bad)) {
+          // Exact path: maximum over every visible key of the wave, then the sums.
+          float mx[PB];
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) mx[pb] = -INFINITY;
+          for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+            for (int pb = 0; pb < PB; ++pb) sm[pb] = 0.f;
+            for (int t = 0; t < TPW; ++t) {
+              const int key0 = key_base + t * 16;
+              if (key0 > last) break;
+              frag_t kf[kS];
+              M::load_k(rsrc, voff + (uint32_t)key0 * row_bytes, kf);  // direct loads: rare path
+              static_for<PB / kHalf>([&](auto h_c) {
+                constexpr int P0 = decltype(h_c)::value * kHalf;
+                f32x4 acc[kHalf];
+                tile_logits<M, PB, P0, kHalf, true>(kf, qf, acc);
+#pragma unroll
+                for (int pb = P0; pb < P0 + kHalf; ++pb) {
+                  const int pi = pos_g[16 * pb + r16];
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) {
+                    const bool v = key0 + 4 * g + e <= pi;
+                    if (pass == 0) mx[pb] = v ? fmaxf(mx[pb], acc[pb - P0][e]) : mx[pb];
+                    else sm[pb] += v ? fast_exp2(fmaf(acc[pb - P0][e], c2, -ref[pb])) : 0.f;
+                  }
+                }
+              });
+            }
+            if (pass == 0) {
+#pragma unroll
+              for (int pb = 0; pb < PB; ++pb) {
+                mx[pb] = max_over_groups(mx[pb]);
+                ref[pb] = mx[pb] != -INFINITY ? mx[pb] * c2 : 0.f;
+              }
+            }
+          }
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb) sm[pb] = sum_over_groups(sm[pb]);
+        }
+        if (g == 0) {
+#pragma unroll
+          for (int pb = 0; pb < PB; ++pb)
+            red[wave][16 * pb + r16] = sm[pb] > 0.f ? make_float2(ref[pb], sm[pb]) : make_float2(-INFINITY, 0.f);
         }
         __syncthreads();
         for (int i = threadIdx.x; i < gn; i += kScoreThreads) {
           float2 r = red[0][i];
 #pragma unroll
-          for (int kk = 1; kk < NK; ++kk) lse_merge(r.x, r.y, red[kk][i].x, red[kk][i].y);
+          for (int w = 1; w < kScoreWaves; ++w) lse_merge(r.x, r.y, red[w][i].x, red[w][i].y);
           store_coherent(part + g0 + i, r);
         }
       }
@@ -596,39 +620,67 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         const int gn = min(kGroup, a.P - g0);
         load_group(g0, gn);
         const int first = pos_g[0], last = pos_g[gn - 1];
-        typename M::frag_t qf[PBW][kS];
+        frag_t qf[PB][kS];
         load_q(gn, qf);
         for (int i = threadIdx.x; i < kGroup; i += kScoreThreads)
           lse_g[i] = i < gn ? load_coherent(lse + (int64_t)bh * a.P + g0 + i) * lse_mul : INFINITY;
         __syncthreads();
-        const float* my_lse = lse_g + ph * kHalfRows;
-        // Column sums over this wave's proxies, accumulated across proxy
-        // groups in the wave's own LDS row (same-wave LDS accesses are ordered).
         // This lane's partial column sums of the last four tiles; every
         // fourth tile they are reduced across lane groups and lane group g
-        // stores tile t - 3 + g.
+        // stores tile t - 3 + g (accumulated across proxy groups in the
+        // wave's own LDS row; same-wave LDS accesses are ordered).
         float cs4[4];
-        auto step2 = [&](int t, const typename M::frag_t (&kf)[kS], auto u_c) {
-          constexpr int u = decltype(u_c)::value;
-          const int key0 = key_base + t * 16;
+        auto mfma2 = [&](int t, const frag_t (&kf)[kS], auto& acc, auto p0_c, auto n_c) {
+          if (key_base + t * 16 > last) return;
+          tile_logits<M, PB, decltype(p0_c)::value, decltype(n_c)::value, false>(kf, qf, acc);
+        };
+        // This lane's share of its key's column sum over blocks [P0, P0 + N);
+        // FULL tiles carry no masking.
+        auto valu2_body = [&](int key0, const auto& acc, auto p0_c, auto n_c, auto full_c) -> float {
+          constexpr int P0 = decltype(p0_c)::value, N = decltype(n_c)::value;
+          constexpr bool FULL = decltype(full_c)::value;
+          const int o = opaque(4 * g);
+          const float* lse_l = lse_g + o;
+          const int* pos_l = pos_g + o;
           float cs = 0.f;
-          if (key0 + 15 <= first) cs = pass2_tile<M, PBW, true>(kf, qf, key0, my_pos, g, r16, c2, my_lse);
-          else if (key0 <= last) cs = pass2_tile<M, PBW, false>(kf, qf, key0, my_pos, g, r16, c2, my_lse);
+#pragma unroll
+          for (int pb = P0; pb < P0 + N; ++pb) {
+            const f32x4 lr = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
+            float x[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb - P0][e], c2, -lr[e]));
+            if constexpr (!FULL) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = key0 + r16 <= pos_l[16 * pb + e] ? x[e] : 0.f;
+            }
+            cs += (x[0] + x[1]) + (x[2] + x[3]);
+          }
+          return cs;
+        };
+        auto valu2 = [&](int t, const auto& acc, auto u_c, auto p0_c, auto n_c) {
+          constexpr int u = decltype(u_c)::value;
+          constexpr int P0 = decltype(p0_c)::value, N = decltype(n_c)::value;
+          const int key0 = key_base + t * 16;
+          float cs = P0 == 0 ? 0.f : cs4[u % 4];
+          if (key0 <= last) {
+            if (key0 + 15 <= first) cs += valu2_body(key0, acc, p0_c, n_c, std::true_type{});
+            else cs += valu2_body(key0, acc, p0_c, n_c, std::false_type{});
+          }
           cs4[u % 4] = cs;
-          if constexpr (u % 4 == 3) {
+          if constexpr (u % 4 == 3 && P0 + N == PB) {
             const float z = colsum4(cs4[0], cs4[1], cs4[2], cs4[3]);
             const int idx = (t - 3) * 16 + lane;
             my_cols[idx] = (g0 == 0 ? 0.f : my_cols[idx]) + z;
           }
         };
-        k_stream(step2);
+        k_stream(mfma2, valu2);
       }
       __syncthreads();
       float* F = s.scores + (int64_t)bh * a.L;
       for (int idx = threadIdx.x; idx < s.chunk_keys; idx += kScoreThreads) {
-        const int pair = idx / kKeysPerPair, j = idx % kKeysPerPair;
+        const int kk = idx / keys_per_wave, j = idx % keys_per_wave;
         const int key = chunk_key0 + idx;
-        if (key < a.L) F[key] = col_lds[2 * pair][j] + col_lds[2 * pair + 1][j];
+        if (key < a.L) F[key] = col_lds[kk][j];
       }
     }
   }
@@ -663,26 +715,31 @@ hipError_t launch_score_t(const ScoreLaunch& L, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <typename T, int D, int PBMAX>
-hipError_t dispatch_pb(const ScoreLaunch& L, hipStream_t stream) {
-  const int need = std::min((L.args.P + 15) / 16, PBMAX);
-  if (need <= 2 || PBMAX == 2) return launch_score_t<T, D, 2>(L, stream);
-  if constexpr (PBMAX >= 4) {
-    if (need <= 4 || PBMAX == 4) return launch_score_t<T, D, 4>(L, stream);
-  }
-  if constexpr (PBMAX >= 8) return launch_score_t<T, D, 8>(L, stream);
-  return hipErrorInvalidValue;
+// Proxy blocks of 16 per group (every wave holds all of them).
+int proxy_blocks(int dtype, int D, int P) {
+  const int need = (P + 15) / 16;
+  if (dtype == 1) return need <= 2 ? 2 : (need <= 4 ? 4 : 8);
+  if (D == 128) return 2;
+  return need <= 2 ? 2 : 4;
 }
 
 }  // namespace
 
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream) {
+  const int pb = proxy_blocks(L.dtype, L.D, L.args.P);
   if (L.dtype == 1) {
-    if (L.D == 128) return dispatch_pb<__bf16, 128, 8>(L, stream);
-    return dispatch_pb<__bf16, 64, 8>(L, stream);
+    if (L.D == 128) {
+      if (pb == 2) return launch_score_t<__bf16, 128, 2>(L, stream);
+      if (pb == 4) return launch_score_t<__bf16, 128, 4>(L, stream);
+      return launch_score_t<__bf16, 128, 8>(L, stream);
+    }
+    if (pb == 2) return launch_score_t<__bf16, 64, 2>(L, stream);
+    if (pb == 4) return launch_score_t<__bf16, 64, 4>(L, stream);
+    return launch_score_t<__bf16, 64, 8>(L, stream);
   }
-  if (L.D == 128) return dispatch_pb<float, 128, 2>(L, stream);
-  return dispatch_pb<float, 64, 4>(L, stream);
+  if (L.D == 128) return launch_score_t<float, 128, 2>(L, stream);
+  if (pb == 2) return launch_score_t<float, 64, 2>(L, stream);
+  return launch_score_t<float, 64, 4>(L, stream);
 }
 
 }  // namespace nacl

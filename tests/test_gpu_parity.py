@@ -102,6 +102,30 @@ def test_score_with_caller_lse():
     check_scores(F.cpu().numpy(), Fr, "caller lse")
 
 
+def test_score_overflow_takes_exact_path():
+    """Pass 1 sums exp2(logit - r) against the maximum r of the first tile of
+    each wave's key range; a later key far above r overflows fp32, and the
+    kernel recomputes that range's sums against its exact maximum.  Here one
+    key per head sits about 180 (natural-log units) above every other logit
+    of its range, so the fast path overflows and the scores are dominated by
+    that key."""
+    B, H, L, D = 1, 2, 3000, 128
+    g = torch.Generator(device="cuda").manual_seed(11)
+    q = torch.randn((B, H, L, D), generator=g, device="cuda")
+    k = torch.randn((B, H, L, D), generator=g, device="cuda")
+    pos = list(range(2900, 3000))
+    q[:, :, 2900:] += 2.0        # proxy rows with a positive mean
+    k[:, 0, 1000] = 8.0          # head 0: a key inside a range, not in its first tile
+    k[:, 1, 2500] = 8.0          # head 1: the same in another item
+    q, k = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    prob = nacl.Problem.from_tensors(q, k, k, pos)
+    F = nacl.score(prob, q, k, nacl.workspace(prob))
+    torch.cuda.synchronize()
+    Fr, _ = proxy_scores(_np(q), _np(k), pos, prob.c.sm_scale)
+    check_scores(F.cpu().numpy(), Fr, "overflow")
+    assert float(F[0, 0, 1000]) > 0.99 * len(pos) and float(F[0, 1, 2500]) > 0.99 * len(pos)
+
+
 def test_score_config_small_and_longbench():
     for key in ("small_f32", "longbench_4k"):
         w = WORKLOADS[key]
