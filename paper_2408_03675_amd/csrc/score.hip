@@ -365,7 +365,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         kBufferRsrcWord3);
 
     // Streams the wave's TPW tiles through its own LDS ring of kDepth slots:
-    // tile t + kDepth - 1 is in flight while tile t is used.  Proxy blocks go
+    // tiles t + 1 .. t + kDepth - 1 are in flight while tile t is used.  Proxy blocks go
     // in batches of kHalf (MFMAs, then their VALU work) so at most kHalf
     // accumulators are live; the other wave on the SIMD fills the MFMA and
     // VALU gaps.  Only this wave touches its ring, so no barrier is involved.
@@ -394,10 +394,13 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         static_for<kUnroll>([&](auto u_c) {
           constexpr int u = decltype(u_c)::value;
           const int tt = t + u;
-          asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KS::kInstr * (kDepth - 2)) : "memory");
+          // The slot of tile tt - 1 was read (and its reads retired) in the
+          // previous step: refill it before waiting, so kDepth - 1 tiles stay
+          // in flight across the wait.
+          KS::issue(rsrc, vo, tile_byte(tt + kDepth - 1), slot(std::integral_constant<int, u + kDepth - 1>{}));
+          asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KS::kInstr * (kDepth - 1)) : "memory");
           frag_t kf[kS];
           KS::template frag<M>(slot(u_c), r16, g, kf);
-          KS::issue(rsrc, vo, tile_byte(tt + kDepth - 1), slot(std::integral_constant<int, u + kDepth - 1>{}));
           static_for<PB / kHalf>([&](auto h_c) {
             using P0 = std::integral_constant<int, decltype(h_c)::value * kHalf>;
             using N = std::integral_constant<int, kHalf>;
