@@ -29,31 +29,27 @@ constexpr int kSelWaves = kSelThreads / kWave;
 // g = -ln(-ln u) in binary64, u = (word + 1/2) / 2^32, word = Philox4x32-10
 // output j mod 4 at counter (j / 4, h, b, layer) under key = seed.
 // MODE selects the log-weight: 0 = F (Softmax(F)), 1 = ln F (weights F),
-// 2 = none (uniform).  One kernel per mode keeps each straight-line.
+// 2 = none (uniform).  One kernel per mode keeps each straight-line.  One
+// thread per token: the two dependent binary64 logarithms are the cost, so
+// every token gets its own thread (the four threads of a Philox block each
+// evaluate the block and keep their word; the integer rounds are cheap next
+// to the logarithms).
 template <int MODE>
 __global__ __launch_bounds__(256) void gumbel_keys_kernel(const float* __restrict__ F, int H, int L,
                                                           uint32_t k0, uint32_t k1, uint32_t layer,
                                                           uint32_t* __restrict__ keys) {
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
-  const int qd = blockIdx.x * 256 + threadIdx.x;
-  const int j0 = qd * 4;
-  if (j0 >= L) return;
-  const U32x4 w = philox4x32_10(U32x4{(uint32_t)qd, (uint32_t)h, (uint32_t)b, layer}, k0, k1);
-  const uint32_t words[4] = {w.x, w.y, w.z, w.w};
-  const float* f = F + (int64_t)bh * L;
-  uint32_t* out = keys + (int64_t)bh * L;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int j = j0 + e;
-    if (j < L) {
-      const double u = ((double)words[e] + 0.5) * 0x1p-32;
-      const double g = -log(-log(u));
-      double key = g;
-      if constexpr (MODE == 0) key = (double)f[j] + g;
-      if constexpr (MODE == 1) key = log((double)f[j]) + g;
-      out[j] = float_order_key((float)key);
-    }
-  }
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= L) return;
+  const U32x4 w = philox4x32_10(U32x4{(uint32_t)(j >> 2), (uint32_t)h, (uint32_t)b, layer}, k0, k1);
+  const int e = j & 3;
+  const uint32_t word = e == 0 ? w.x : (e == 1 ? w.y : (e == 2 ? w.z : w.w));
+  const double u = ((double)word + 0.5) * 0x1p-32;
+  const double g = -log(-log(u));
+  double key = g;
+  if constexpr (MODE == 0) key = (double)F[(int64_t)bh * L + j] + g;
+  if constexpr (MODE == 1) key = log((double)F[(int64_t)bh * L + j]) + g;
+  keys[(int64_t)bh * L + j] = float_order_key((float)key);
 }
 
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane) {
@@ -161,7 +157,9 @@ __device__ void radix_select(const Get& get, int L, uint32_t k, const SelScratch
 
 // Sets, in out_bits, the bit of every token with key >= T: the top k when
 // every key equal to T belongs to it.  Each wave covers 64 consecutive tokens
-// per step and writes their two bitmap words from a ballot.
+// per step; lanes 0 and 32 OR the two words of the ballot into the bitmap
+// (the words of a step belong to that wave alone, so no atomics are needed),
+// and the four steps of an iteration keep their loads and updates independent.
 template <class Get>
 __device__ void mark_at_least(const Get& get, int L, uint32_t T, uint32_t* out_bits) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -176,9 +174,10 @@ __device__ void mark_at_least(const Get& get, int L, uint32_t T, uint32_t* out_b
     for (int u = 0; u < 4; ++u) {
       const int base = b0 + u * kSelThreads;
       const uint64_t m = __ballot(take[u]);
-      if (lane == 0 && base < L) {
-        out_bits[base >> 5] |= (uint32_t)m;
-        if (base + 32 < L) out_bits[(base >> 5) + 1] |= (uint32_t)(m >> 32);
+      const int word = (base >> 5) + (lane >> 5);
+      if ((lane & 31) == 0 && base + (lane & 32) < L) {
+        const uint32_t bits = (lane & 32) ? (uint32_t)(m >> 32) : (uint32_t)m;
+        if (bits) out_bits[word] |= bits;
       }
     }
   }
@@ -355,7 +354,7 @@ constexpr size_t kMaxLds = 160 * 1024;
 hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
   const int BH = a.B * a.H;
   if (a.Cr > 0) {
-    dim3 gk(((a.L + 3) / 4 + 255) / 256, BH);
+    dim3 gk((a.L + 255) / 256, BH);
     const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFu), k1 = (uint32_t)(a.seed >> 32);
     if (a.sampling == 0)
       hipLaunchKernelGGL(gumbel_keys_kernel<0>, gk, dim3(256), 0, stream, a.scores, a.H, a.L, k0, k1,
