@@ -128,7 +128,15 @@ int nacl_compact(const nacl_problem* p, const void* k, const void* v,
                  void* stream);
 
 /* The whole step for one layer: score, select, compact on one stream
- * (Algorithm 1, encoding phase).  Arguments as above. */
+ * (Algorithm 1, encoding phase).  Arguments as above.
+ * Generation-phase eviction (Section 3, "Generation Phase Eviction"; the
+ * Generation function of Algorithm 1) is the same call at decode shapes:
+ * every m steps, with the cache holding C + m entries, pass L = C + m, the
+ * current token as the only proxy (proxy_pos = {L - 1}, n_protect = 1), and
+ * its query as a [B,H,1,D] tensor with q_stride[2] = 0; k_out, v_out receive
+ * the C kept entries (a second buffer: they may not alias k, v).  Use a
+ * different seed per eviction round so the random draws differ between
+ * rounds. */
 int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* v,
                int32_t C, int32_t Cr, int32_t sampling, uint64_t seed, uint32_t layer,
                float* scores, int32_t* keep_idx, void* k_out, void* v_out,
