@@ -82,7 +82,7 @@ struct SelectLaunch {
 };
 
 hipError_t launch_select(const SelectLaunch& L, hipStream_t stream);
-size_t select_lds_bytes(int L, bool keys_in_lds);
+size_t select_lds_bytes(int L);
 
 struct CompactLaunch {
   int B, H, C, row_vecs;        // row_vecs = D * elt / 16

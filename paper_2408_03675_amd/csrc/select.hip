@@ -25,64 +25,146 @@ namespace nacl {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
 
+// ln(x) in binary64 for x >= 0 (ln 0 = -inf, ln inf = inf), to within a
+// few units in the last place: x = m 2^e with m in [sqrt(1/2), sqrt(2)),
+// ln m = 2 atanh(s) with s = (m - 1) / (m + 1), |s| < 0.172, summed as the
+// odd series 2 s (1 + s^2/3 + s^4/5 + ... + s^20/21) (the next term is
+// below 2^-59 relative), and e ln 2 added in two parts (ln 2 rounded to
+// binary64 and the rest).  The quotient takes a hardware reciprocal, two
+// Newton steps and one residual correction.  The keys are rounded to
+// binary32 afterwards, so a few binary64 units never matter except for a
+// key within that distance of a binary32 rounding boundary.
+__device__ __forceinline__ double ln_f64(double x) {
+  constexpr double kLn2 = 0.6931471805599453094172321;         // rounded to binary64
+  constexpr double kLn2Rest = 2.319046813846299558e-17;        // ln 2 - kLn2
+  constexpr double kSqrtHalf = 0.70710678118654752440;
+  double m = __builtin_amdgcn_frexp_mant(x);                   // [1/2, 1)
+  int e = __builtin_amdgcn_frexp_exp(x);
+  if (m < kSqrtHalf) {
+    m *= 2.0;
+    --e;
+  }
+  const double f = m - 1.0;                                    // exact
+  const double d = f + 2.0;
+  double r = __builtin_amdgcn_rcp(d);
+  r = fma(r, fma(-d, r, 1.0), r);
+  r = fma(r, fma(-d, r, 1.0), r);
+  double s = f * r;
+  s = fma(fma(-s, d, f), r, s);
+  const double z = s * s;
+  double q = 1.0 / 21;
+  q = fma(q, z, 1.0 / 19);
+  q = fma(q, z, 1.0 / 17);
+  q = fma(q, z, 1.0 / 15);
+  q = fma(q, z, 1.0 / 13);
+  q = fma(q, z, 1.0 / 11);
+  q = fma(q, z, 1.0 / 9);
+  q = fma(q, z, 1.0 / 7);
+  q = fma(q, z, 1.0 / 5);
+  q = fma(q, z, 1.0 / 3);
+  const double s2 = 2.0 * s;
+  const double lnm = fma(s2 * z, q, s2);
+  const double ed = (double)e;
+  const double p = ed * kLn2;
+  const double perr = fma(ed, kLn2, -p);                       // exact rounding error of p
+  const double res = p + (lnm + fma(ed, kLn2Rest, perr));
+  if (x == 0.0) return -INFINITY;
+  if (x == INFINITY) return INFINITY;
+  return res;
+}
+
 // Gumbel keys of every token: key = binary32(logw + g) with
 // g = -ln(-ln u) in binary64, u = (word + 1/2) / 2^32, word = Philox4x32-10
 // output j mod 4 at counter (j / 4, h, b, layer) under key = seed.
 // MODE selects the log-weight: 0 = F (Softmax(F)), 1 = ln F (weights F),
 // 2 = none (uniform).  One kernel per mode keeps each straight-line.  One
-// thread per token: the two dependent binary64 logarithms are the cost, so
-// every token gets its own thread (the four threads of a Philox block each
-// evaluate the block and keep their word; the integer rounds are cheap next
-// to the logarithms).
+// thread per Philox block, i.e. four consecutive tokens: 16-byte loads and
+// stores when the rows allow (vec), the block evaluated once.
 template <int MODE>
 __global__ __launch_bounds__(256) void gumbel_keys_kernel(const float* __restrict__ F, int H, int L,
-                                                          uint32_t k0, uint32_t k1, uint32_t layer,
+                                                          uint32_t k0, uint32_t k1, uint32_t layer, int vec,
                                                           uint32_t* __restrict__ keys) {
   const int bh = blockIdx.y, b = bh / H, h = bh % H;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= L) return;
-  const U32x4 w = philox4x32_10(U32x4{(uint32_t)(j >> 2), (uint32_t)h, (uint32_t)b, layer}, k0, k1);
-  const int e = j & 3;
-  const uint32_t word = e == 0 ? w.x : (e == 1 ? w.y : (e == 2 ? w.z : w.w));
-  const double u = ((double)word + 0.5) * 0x1p-32;
-  const double g = -log(-log(u));
-  double key = g;
-  if constexpr (MODE == 0) key = (double)F[(int64_t)bh * L + j] + g;
-  if constexpr (MODE == 1) key = log((double)F[(int64_t)bh * L + j]) + g;
-  keys[(int64_t)bh * L + j] = float_order_key((float)key);
+  const int blk = blockIdx.x * 256 + threadIdx.x;
+  const int j0 = 4 * blk;
+  if (j0 >= L) return;
+  const float* f = F + (int64_t)bh * L + j0;
+  uint32_t* out = keys + (int64_t)bh * L + j0;
+  const int n = min(4, L - j0);
+  float fv[4] = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (MODE != 2) {
+    if (vec) {
+      const float4 v4 = *reinterpret_cast<const float4*>(f);
+      fv[0] = v4.x;
+      fv[1] = v4.y;
+      fv[2] = v4.z;
+      fv[3] = v4.w;
+    } else {
+      for (int e = 0; e < n; ++e) fv[e] = f[e];
+    }
+  }
+  const U32x4 w = philox4x32_10(U32x4{(uint32_t)blk, (uint32_t)h, (uint32_t)b, layer}, k0, k1);
+  const uint32_t word[4] = {w.x, w.y, w.z, w.w};
+  uint32_t kv[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const double u = ((double)word[e] + 0.5) * 0x1p-32;
+    const double g = -ln_f64(-ln_f64(u));
+    double key = g;
+    if constexpr (MODE == 0) key = (double)fv[e] + g;
+    if constexpr (MODE == 1) key = ln_f64((double)fv[e]) + g;
+    kv[e] = float_order_key((float)key);
+  }
+  if (vec) {
+    *reinterpret_cast<uint4*>(out) = uint4{kv[0], kv[1], kv[2], kv[3]};
+  } else {
+    for (int e = 0; e < n; ++e) out[e] = kv[e];
+  }
 }
 
-__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane) {
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const uint32_t y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
+// Inclusive prefix sum over the wave by DPP: shifts of 1, 2, 4 and 8 lanes
+// within each 16-lane row, then the last lane of a row broadcast into the
+// next row (rows 1 and 3) and lane 31 into the upper half (rows 2 and 3).
+// Lanes a shift leaves without a source add 0.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_or_zero(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xf, false);
+}
+
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  x += dpp_or_zero<0x111, 0xf>(x);  // row_shr:1
+  x += dpp_or_zero<0x112, 0xf>(x);  // row_shr:2
+  x += dpp_or_zero<0x114, 0xf>(x);  // row_shr:4
+  x += dpp_or_zero<0x118, 0xf>(x);  // row_shr:8
+  x += dpp_or_zero<0x142, 0xa>(x);  // row_bcast:15
+  x += dpp_or_zero<0x143, 0xc>(x);  // row_bcast:31
   return x;
 }
 
 // Exclusive prefix sum of v over the work-group in thread order.  scan_buf
-// holds 2 * kSelWaves words of LDS.
+// holds 2 * kSelWaves words of LDS: the wave totals, then their scan.  A
+// call may follow another directly: a thread only writes the first half
+// after every thread has left the previous call's second barrier, and the
+// second half after every thread has read the previous call's result.
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scan_buf) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t x = wave_inclusive_scan(v, lane);
+  const uint32_t x = wave_inclusive_scan(v);
   if (lane == kWave - 1) scan_buf[wave] = x;
   __syncthreads();
   if (wave == 0) {
     uint32_t t = lane < kSelWaves ? scan_buf[lane] : 0u;
-    t = wave_inclusive_scan(t, lane);
+    t = wave_inclusive_scan(t);
     if (lane < kSelWaves) scan_buf[kSelWaves + lane] = t;
   }
   __syncthreads();
   const uint32_t base = wave ? scan_buf[kSelWaves + wave - 1] : 0u;
-  __syncthreads();
   return base + x - v;
 }
 
 struct SelScratch {
-  uint32_t* hist;   // kHistBins
+  uint32_t* hist;   // kHistBins, all zero between radix passes
   uint32_t* scan;   // 2 * kSelWaves
-  uint32_t* shv;    // 4
+  uint32_t* shv;    // 3: radix pick results
 };
 
 // Radix select digits, most significant first: 12 + 12 + 8 bits.  The wide
@@ -93,8 +175,52 @@ constexpr int kHistBins = 4096;
 constexpr int kDigitShift[3] = {20, 8, 0};
 constexpr int kDigitBits[3] = {12, 12, 8};
 
+// After a histogram pass over the digit at `shift`: the digit at which the
+// count from the top reaches kr, appended to prefix; kr becomes the rank
+// within that digit's keys and n_eq their number.  Thread t owns bins
+// nbins-1-per*t down to nbins-per-per*t and zeroes them once read, so the
+// histogram is all zero again for the next pass.
+__device__ void radix_pick(int shift, int nbins, const SelScratch& s, uint32_t& prefix, uint32_t& kr,
+                           uint32_t& n_eq) {
+  const int tid = threadIdx.x;
+  const int per = (nbins + kSelThreads - 1) / kSelThreads;  // 4 or 1
+  uint32_t c[4] = {0u, 0u, 0u, 0u}, local = 0u;
+#pragma unroll
+  for (int qq = 0; qq < 4; ++qq) {
+    const int b = nbins - 1 - per * tid - qq;
+    if (qq < per && b >= 0) {
+      c[qq] = s.hist[b];
+      s.hist[b] = 0u;
+    }
+    local += c[qq];
+  }
+  const uint32_t excl = block_exclusive_scan(local, s.scan);
+  if (excl < kr && kr <= excl + local) {
+    uint32_t cum = excl;
+    for (int qq = 0; qq < per; ++qq) {
+      if (cum + c[qq] >= kr) {
+        s.shv[0] = prefix | ((uint32_t)(nbins - 1 - per * tid - qq) << shift);
+        s.shv[1] = kr - cum;
+        s.shv[2] = c[qq];
+        break;
+      }
+      cum += c[qq];
+    }
+  }
+  // The next write of shv follows the next pass's histogram barrier, which
+  // every thread reaches only after reading these values.
+  __syncthreads();
+  prefix = s.shv[0];
+  kr = s.shv[1];
+  n_eq = s.shv[2];
+}
+
 // k-th largest key T (1 <= k <= number of keys), the number `need` of keys
 // equal to T that belong to the top k, and the number n_eq of keys equal to T.
+// get(j) reads key j.  A key of 0 marks an excluded token and is never
+// counted: the first pass skips it, and later prefixes never match it (an
+// order key below 2^20 would be a NaN, so every real key has a nonzero
+// first digit).
 template <class Get>
 __device__ void radix_select(const Get& get, int L, uint32_t k, const SelScratch& s, uint32_t& T,
                              uint32_t& need, uint32_t& n_eq) {
@@ -103,11 +229,8 @@ __device__ void radix_select(const Get& get, int L, uint32_t k, const SelScratch
 #pragma unroll
   for (int pass = 0; pass < 3; ++pass) {
     const int shift = kDigitShift[pass];
-    const int nbins = 1 << kDigitBits[pass];
-    const uint32_t dmask = (uint32_t)nbins - 1u;
+    const uint32_t dmask = (1u << kDigitBits[pass]) - 1u;
     const uint32_t hm = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + kDigitBits[pass]));
-    for (int i = tid; i < nbins; i += kSelThreads) s.hist[i] = 0u;
-    __syncthreads();
     // Eight keys per thread in flight before their counter updates.
     for (int j0 = tid; j0 < L; j0 += 8 * kSelThreads) {
       uint32_t kv[8];
@@ -117,49 +240,44 @@ __device__ void radix_select(const Get& get, int L, uint32_t k, const SelScratch
         kv[u] = j < L ? get(j) : 0u;
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 + u * kSelThreads;
-        if (j < L && ((kv[u] ^ prefix) & hm) == 0u) atomicAdd(&s.hist[(kv[u] >> shift) & dmask], 1u);
-      }
+      for (int u = 0; u < 8; ++u)
+        if (pass == 0 ? kv[u] != 0u : ((kv[u] ^ prefix) & hm) == 0u)
+          atomicAdd(&s.hist[(kv[u] >> shift) & dmask], 1u);
     }
     __syncthreads();
-    // Counts from the top: thread t owns bins nbins-1-4t down to nbins-4-4t.
-    const int per = (nbins + kSelThreads - 1) / kSelThreads;  // 4 or 1
-    uint32_t c[4] = {0u, 0u, 0u, 0u}, local = 0u;
-#pragma unroll
-    for (int qq = 0; qq < 4; ++qq) {
-      const int b = nbins - 1 - per * tid - qq;
-      if (qq < per && b >= 0) c[qq] = s.hist[b];
-      local += c[qq];
-    }
-    const uint32_t excl = block_exclusive_scan(local, s.scan);
-    if (excl < kr && kr <= excl + local) {
-      uint32_t cum = excl;
-      for (int qq = 0; qq < per; ++qq) {
-        if (cum + c[qq] >= kr) {
-          s.shv[0] = prefix | ((uint32_t)(nbins - 1 - per * tid - qq) << shift);
-          s.shv[1] = kr - cum;
-          s.shv[2] = c[qq];
-          break;
-        }
-        cum += c[qq];
-      }
-    }
-    __syncthreads();
-    prefix = s.shv[0];
-    kr = s.shv[1];
-    n_eq = s.shv[2];
-    __syncthreads();
+    radix_pick(shift, 1 << kDigitBits[pass], s, prefix, kr, n_eq);
   }
   T = prefix;
   need = kr;
 }
 
-// Sets, in out_bits, the bit of every token with key >= T: the top k when
-// every key equal to T belongs to it.  Each wave covers 64 consecutive tokens
-// per step; lanes 0 and 32 OR the two words of the ballot into the bitmap
-// (the words of a step belong to that wave alone, so no atomics are needed),
-// and the four steps of an iteration keep their loads and updates independent.
+// The same over keys held in registers: key[i] belongs to token
+// i * kSelThreads + threadIdx.x (0 past the end of the head or excluded).
+template <int NR>
+__device__ __forceinline__ void radix_select_regs(const uint32_t (&key)[NR], uint32_t k, const SelScratch& s,
+                                                  uint32_t& T, uint32_t& need, uint32_t& n_eq) {
+  uint32_t prefix = 0u, kr = k;
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = kDigitShift[pass];
+    const uint32_t dmask = (1u << kDigitBits[pass]) - 1u;
+    const uint32_t hm = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + kDigitBits[pass]));
+#pragma unroll
+    for (int i = 0; i < NR; ++i)
+      if (pass == 0 ? key[i] != 0u : ((key[i] ^ prefix) & hm) == 0u)
+        atomicAdd(&s.hist[(key[i] >> shift) & dmask], 1u);
+    __syncthreads();
+    radix_pick(shift, 1 << kDigitBits[pass], s, prefix, kr, n_eq);
+  }
+  T = prefix;
+  need = kr;
+}
+
+// Sets, in out_bits, the bit of every token with key >= T (T > 0): the top k
+// when every key equal to T belongs to it.  Each wave covers 64 consecutive
+// tokens per step; lanes 0 and 32 OR the two words of the ballot into the
+// bitmap with LDS atomics that return nothing (no wait on the old word), and
+// the four steps of an iteration keep their loads and updates independent.
 template <class Get>
 __device__ void mark_at_least(const Get& get, int L, uint32_t T, uint32_t* out_bits) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -177,8 +295,24 @@ __device__ void mark_at_least(const Get& get, int L, uint32_t T, uint32_t* out_b
       const int word = (base >> 5) + (lane >> 5);
       if ((lane & 31) == 0 && base + (lane & 32) < L) {
         const uint32_t bits = (lane & 32) ? (uint32_t)(m >> 32) : (uint32_t)m;
-        if (bits) out_bits[word] |= bits;
+        if (bits) atomicOr(&out_bits[word], bits);
       }
+    }
+  }
+  __syncthreads();
+}
+
+// The same over keys in registers (same token mapping as radix_select_regs).
+template <int NR>
+__device__ __forceinline__ void mark_at_least_regs(const uint32_t (&key)[NR], int L, uint32_t T, uint32_t* out_bits) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    const int base = i * kSelThreads + wave * 64;
+    const uint64_t m = __ballot(key[i] >= T);
+    if ((lane & 31) == 0 && base + (lane & 32) < L) {
+      const uint32_t bits = (lane & 32) ? (uint32_t)(m >> 32) : (uint32_t)m;
+      if (bits) atomicOr(&out_bits[(base >> 5) + (lane >> 5)], bits);
     }
   }
   __syncthreads();
@@ -229,50 +363,156 @@ __device__ void select_top(const Get& get, int L, int nwords, int seg_words, uin
   else mark_top(get, L, nwords, seg_words, T, need, out_bits, s.scan);
 }
 
-// keys_lds[j] = f(j, src[j]) for the whole head: 16-byte loads, eight per
-// thread in flight (src is 16-byte aligned when L % 4 == 0; otherwise
-// 4-byte loads).
-template <class F>
-__device__ void stage_keys(int L, const uint32_t* src, uint32_t* keys_lds, const F& f) {
-  if ((L & 3) == 0) {
-    const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
-    const int n4 = L >> 2;
-    for (int i0 = threadIdx.x; i0 < n4; i0 += 8 * kSelThreads) {
-      u32x4 v[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + u * kSelThreads;
-        v[u] = i < n4 ? s4[i] : u32x4{0u, 0u, 0u, 0u};
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + u * kSelThreads;
-        if (i < n4) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) keys_lds[4 * i + e] = f(4 * i + e, v[u][e]);
-        }
-      }
+// keep = the set bits of a | b in ascending order, C of them: ranks by an
+// ordered scan of the bitmap words (thread t owns words [t * seg_words,
+// (t + 1) * seg_words)), the list assembled in `list` (LDS, then copied out
+// with coalesced stores, or keep itself).
+__device__ void assemble_keep(const uint32_t* a_bits, const uint32_t* b_bits, int nwords, int seg_words, int C,
+                              const SelScratch& s, int32_t* list, int32_t* keep) {
+  const int tid = threadIdx.x;
+  const int w0 = tid * seg_words;
+  const int w1 = min(w0 + seg_words, nwords);
+  uint32_t cnt = 0;
+  for (int w = w0; w < w1; ++w) cnt += __popc(a_bits[w] | b_bits[w]);
+  uint32_t out = block_exclusive_scan(cnt, s.scan);
+  for (int w = w0; w < w1; ++w) {
+    uint32_t bits = a_bits[w] | b_bits[w];
+    while (bits) {
+      const int bit = __ffs(bits) - 1;
+      if (out < (uint32_t)C) list[out] = w * 32 + bit;  // |keep| == C by construction
+      ++out;
+      bits &= bits - 1;
     }
-  } else {
-    for (int j = threadIdx.x; j < L; j += kSelThreads) keys_lds[j] = f(j, src[j]);
   }
-  __syncthreads();
+  if (list != keep) {
+    __syncthreads();
+    for (int c = tid; c < C; c += kSelThreads) keep[c] = list[c];
+  }
 }
 
-// KEYS_IN_LDS: the head's keys live in LDS (L * 4 bytes), loaded once per
-// selection; otherwise every radix pass re-reads them from global memory
-// (L2-resident) for heads too long for LDS.
-template <bool KEYS_IN_LDS>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
+// Heads of up to kRegMaxL tokens: every thread holds the scores and Gumbel
+// keys of tokens tid + i * kSelThreads (i < kRegKeys) in registers, both
+// loaded at the start so the Gumbel keys arrive while the top-Cp search
+// runs.  Radix passes and ballot marking then touch LDS only for the
+// histogram and the bitmaps.  LDS: L words (the keys for the ordered tie
+// scan, then the keep list), two bitmaps, the histogram.
+constexpr int kRegKeys = 32;
+constexpr int kRegMaxL = kRegKeys * kSelThreads;
+
+// The top k of the register keys into out_bits; returns the k-th largest
+// key T when the top k are exactly the keys >= T (then a token's membership
+// is a register compare), else 0 (ties at T split by index).
+template <int NR>
+__device__ __forceinline__ uint32_t top_regs(const uint32_t (&key)[NR], int L, uint32_t k, const SelScratch& s,
+                                             uint32_t* keys_lds, uint32_t* out_bits) {
+  uint32_t T, need, n_eq;
+  radix_select_regs(key, k, s, T, need, n_eq);
+  if (need == n_eq) {
+    mark_at_least_regs(key, L, T, out_bits);
+    return T;
+  } else {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const int j = i * kSelThreads + (int)threadIdx.x;
+      if (j < L) keys_lds[j] = key[i];
+    }
+    __syncthreads();
+    mark_top([&](int j) { return keys_lds[j]; }, L, (L + 31) / 32, 1, T, need, out_bits, s.scan);
+    return 0u;
+  }
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a) {
+  extern __shared__ uint32_t smem[];
+  const int L = a.L;
+  const int nwords = (L + 31) / 32;  // <= kSelThreads
+  uint32_t* keys_lds = smem;
+  uint32_t* fixed = smem + L;        // Pi, then Pi | u_score
+  uint32_t* rnd = fixed + nwords;    // u_random
+  SelScratch s;
+  s.hist = rnd + nwords;
+  s.scan = s.hist + kHistBins;
+  s.shv = s.scan + 2 * kSelWaves;
+
+  const int tid = threadIdx.x;
+  const int bh = blockIdx.x;
+  const uint32_t* fbits = reinterpret_cast<const uint32_t*>(a.scores) + (int64_t)bh * L;
+  const uint32_t* gsrc = a.keys2 + (int64_t)bh * L;
+
+  // The first protected position is loaded ahead of the keys, so that using
+  // it does not wait for them.
+  const int pbase = a.P - a.n_protect;
+  const int p0 = pbase + tid < a.P ? a.pos[pbase + tid] : -1;
+
+  // Past the end of the head the loads repeat the last token (masked below),
+  // so every load is unconditional and all of them are in flight at once.
+  uint32_t fk[kRegKeys], gk[kRegKeys];
+  if (a.Cp > 0) {
+#pragma unroll
+    for (int i = 0; i < kRegKeys; ++i) fk[i] = fbits[min(i * kSelThreads + tid, L - 1)];
+  }
+  if (a.Cr > 0) {
+#pragma unroll
+    for (int i = 0; i < kRegKeys; ++i) gk[i] = gsrc[min(i * kSelThreads + tid, L - 1)];
+  }
+
+  if (tid < nwords) {
+    fixed[tid] = 0u;
+    rnd[tid] = 0u;
+  }
+  for (int i = tid; i < kHistBins; i += kSelThreads) s.hist[i] = 0u;
+  __syncthreads();
+  if (p0 >= 0) atomicOr(&fixed[p0 >> 5], 1u << (p0 & 31));
+  for (int i = pbase + tid + kSelThreads; i < a.P; i += kSelThreads) {
+    const int j = a.pos[i];
+    atomicOr(&fixed[j >> 5], 1u << (j & 31));
+  }
+  __syncthreads();
+  auto is_fixed = [&](int j) -> bool { return ((fixed[j >> 5] >> (j & 31)) & 1u) != 0u; };
+
+  // u_score: top-Cp of F over R = [0, L) \ Pi, marked into `fixed`.
+  uint32_t T1 = 0u;
+  if (a.Cp > 0) {
+#pragma unroll
+    for (int i = 0; i < kRegKeys; ++i) {
+      const int j = i * kSelThreads + tid;
+      fk[i] = (j < L && !is_fixed(j)) ? float_order_key(__uint_as_float(fk[i])) : 0u;
+    }
+    T1 = top_regs(fk, L, (uint32_t)a.Cp, s, keys_lds, fixed);
+  }
+
+  // u_random: top-Cr of the Gumbel keys over R \ u_score.  Excluded are the
+  // tokens past the end, Pi (score key 0) and u_score (score key >= T1)
+  // when u_score is exactly the keys >= T1; otherwise the bitmap says.
+  if (a.Cr > 0) {
+    if (T1) {
+#pragma unroll
+      for (int i = 0; i < kRegKeys; ++i)
+        if (fk[i] == 0u || fk[i] >= T1) gk[i] = 0u;
+    } else {
+#pragma unroll
+      for (int i = 0; i < kRegKeys; ++i) {
+        const int j = i * kSelThreads + tid;
+        if (j >= L || is_fixed(j)) gk[i] = 0u;
+      }
+    }
+    top_regs(gk, L, (uint32_t)a.Cr, s, keys_lds, rnd);
+  }
+
+  assemble_keep(fixed, rnd, nwords, 1, a.C, s, reinterpret_cast<int32_t*>(keys_lds), a.keep + (int64_t)bh * a.C);
+}
+
+// Longer heads: every radix pass re-reads the keys from global memory
+// (L2-resident); the bitmaps and the histogram stay in LDS.
+__global__ __launch_bounds__(kSelThreads) void select_kernel_global(SelectLaunch a) {
   extern __shared__ uint32_t smem[];
   const int L = a.L;
   const int nwords = (L + 31) / 32;
   const int seg_words = (nwords + kSelThreads - 1) / kSelThreads;
-  uint32_t* keys_lds = smem;
-  uint32_t* prot = smem + (KEYS_IN_LDS ? L : 0);
-  uint32_t* sel = prot + nwords;
+  uint32_t* fixed = smem;            // Pi, then Pi | u_score
+  uint32_t* rnd = fixed + nwords;    // u_random
   SelScratch s;
-  s.hist = sel + nwords;
+  s.hist = rnd + nwords;
   s.scan = s.hist + kHistBins;
   s.shv = s.scan + 2 * kSelWaves;
 
@@ -282,101 +522,66 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
   const uint32_t* keys = a.keys2 + (int64_t)bh * L;
 
   for (int w = tid; w < nwords; w += kSelThreads) {
-    prot[w] = 0u;
-    sel[w] = 0u;
+    fixed[w] = 0u;
+    rnd[w] = 0u;
   }
+  for (int i = tid; i < kHistBins; i += kSelThreads) s.hist[i] = 0u;
   __syncthreads();
   for (int i = a.P - a.n_protect + tid; i < a.P; i += kSelThreads) {
     const int j = a.pos[i];
-    atomicOr(&prot[j >> 5], 1u << (j & 31));
+    atomicOr(&fixed[j >> 5], 1u << (j & 31));
   }
   __syncthreads();
-  auto excluded = [&](int j) -> bool { return (((prot[j >> 5] | sel[j >> 5]) >> (j & 31)) & 1u) != 0u; };
 
-  // u_score: top-Cp of F over R.
-  if (a.Cp > 0) {
-    if constexpr (KEYS_IN_LDS) {
-      stage_keys(L, reinterpret_cast<const uint32_t*>(f), keys_lds,
-                 [&](int j, uint32_t bits) { return excluded(j) ? 0u : float_order_key(__uint_as_float(bits)); });
-      select_top([&](int j) { return keys_lds[j]; }, L, nwords, seg_words, (uint32_t)a.Cp, s, sel);
-    } else {
-      select_top([&](int j) { return ((prot[j >> 5] >> (j & 31)) & 1u) ? 0u : float_order_key(f[j]); }, L,
-                 nwords, seg_words, (uint32_t)a.Cp, s, sel);
-    }
-  }
+  // u_score.  Reads `fixed` inside its own marking: a token's bit is read
+  // before its word is updated, and a pick is never an excluded token.
+  if (a.Cp > 0)
+    select_top([&](int j) { return ((fixed[j >> 5] >> (j & 31)) & 1u) ? 0u : float_order_key(f[j]); }, L,
+               nwords, seg_words, (uint32_t)a.Cp, s, fixed);
+  // u_random over R \ u_score.
+  if (a.Cr > 0)
+    select_top([&](int j) { return ((fixed[j >> 5] >> (j & 31)) & 1u) ? 0u : keys[j]; }, L, nwords,
+               seg_words, (uint32_t)a.Cr, s, rnd);
 
-  // u_random: top-Cr of the Gumbel keys over R \ u_score.
-  if (a.Cr > 0) {
-    if constexpr (KEYS_IN_LDS) {
-      stage_keys(L, keys, keys_lds, [&](int j, uint32_t key) { return excluded(j) ? 0u : key; });
-      select_top([&](int j) { return keys_lds[j]; }, L, nwords, seg_words, (uint32_t)a.Cr, s, sel);
-    } else {
-      // Reads sel inside the marking of sel: a token's own bit is read before
-      // its word is updated, and random picks are never excluded tokens.
-      select_top([&](int j) { return excluded(j) ? 0u : keys[j]; }, L, nwords, seg_words, (uint32_t)a.Cr, s,
-                 sel);
-    }
-  }
-
-  // keep = Pi | u_score | u_random, in ascending order: ranks by an ordered
-  // scan of the bitmap words, the list assembled in LDS (over the keys when
-  // they live there), then copied out with coalesced stores.
-  const int w0 = tid * seg_words;
-  const int w1 = min(w0 + seg_words, nwords);
-  uint32_t cnt = 0;
-  for (int w = w0; w < w1; ++w) cnt += __popc(sel[w] | prot[w]);
-  uint32_t out = block_exclusive_scan(cnt, s.scan);
-  int32_t* keep = a.keep + (int64_t)bh * a.C;
-  int32_t* list = KEYS_IN_LDS ? reinterpret_cast<int32_t*>(keys_lds) : keep;
-  for (int w = w0; w < w1; ++w) {
-    uint32_t bits = sel[w] | prot[w];
-    while (bits) {
-      const int bit = __ffs(bits) - 1;
-      if (out < (uint32_t)a.C) list[out] = w * 32 + bit;  // |keep| == C by construction
-      ++out;
-      bits &= bits - 1;
-    }
-  }
-  if constexpr (KEYS_IN_LDS) {
-    __syncthreads();
-    for (int c = tid; c < a.C; c += kSelThreads) keep[c] = list[c];
-  }
+  assemble_keep(fixed, rnd, nwords, seg_words, a.C, s, a.keep + (int64_t)bh * a.C,
+                a.keep + (int64_t)bh * a.C);
 }
 
-// LDS bytes of select_kernel: bitmaps + histograms (+ keys when in LDS).
-size_t select_lds_bytes(int L, bool keys_in_lds) {
+// LDS bytes of the selection for a head of L tokens.
+size_t select_lds_bytes(int L) {
   const size_t nwords = ((size_t)L + 31) / 32;
-  return ((keys_in_lds ? (size_t)L : 0) + 2 * nwords + kHistBins + 2 * kSelWaves + 4) * sizeof(uint32_t);
+  const size_t keys = L <= kRegMaxL ? (size_t)L : 0;
+  return (keys + 2 * nwords + kHistBins + 2 * kSelWaves + 3) * sizeof(uint32_t);
 }
-
-constexpr size_t kMaxLds = 160 * 1024;
 
 hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
   const int BH = a.B * a.H;
   if (a.Cr > 0) {
-    dim3 gk((a.L + 255) / 256, BH);
+    dim3 gk((a.L + 1023) / 1024, BH);
     const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFu), k1 = (uint32_t)(a.seed >> 32);
+    // 16-byte rows: every row start 16-byte aligned (the workspace always is).
+    const int vec = (a.L % 4 == 0) && ((uintptr_t)a.scores % 16 == 0) && ((uintptr_t)a.keys2 % 16 == 0);
     if (a.sampling == 0)
       hipLaunchKernelGGL(gumbel_keys_kernel<0>, gk, dim3(256), 0, stream, a.scores, a.H, a.L, k0, k1,
-                         a.layer, a.keys2);
+                         a.layer, vec, a.keys2);
     else if (a.sampling == 1)
       hipLaunchKernelGGL(gumbel_keys_kernel<1>, gk, dim3(256), 0, stream, a.scores, a.H, a.L, k0, k1,
-                         a.layer, a.keys2);
+                         a.layer, vec, a.keys2);
     else
       hipLaunchKernelGGL(gumbel_keys_kernel<2>, gk, dim3(256), 0, stream, a.scores, a.H, a.L, k0, k1,
-                         a.layer, a.keys2);
+                         a.layer, vec, a.keys2);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const bool in_lds = select_lds_bytes(a.L, true) <= kMaxLds;
-  const size_t lds = select_lds_bytes(a.L, in_lds);
-  const void* fn = in_lds ? (const void*)select_kernel<true> : (const void*)select_kernel<false>;
+  const bool regs = a.L <= kRegMaxL;
+  const size_t lds = select_lds_bytes(a.L);
+  const void* fn = regs ? (const void*)select_kernel_regs : (const void*)select_kernel_global;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  if (in_lds) hipLaunchKernelGGL(select_kernel<true>, dim3(BH), dim3(kSelThreads), lds, stream, a);
-  else hipLaunchKernelGGL(select_kernel<false>, dim3(BH), dim3(kSelThreads), lds, stream, a);
+  if (regs) hipLaunchKernelGGL(select_kernel_regs, dim3(BH), dim3(kSelThreads), lds, stream, a);
+  else hipLaunchKernelGGL(select_kernel_global, dim3(BH), dim3(kSelThreads), lds, stream, a);
   return hipGetLastError();
 }
 

@@ -150,7 +150,7 @@ SELECT_CASES = [
     ("ties_heavy", 5000, 8, 8, 1000, 300, SAMPLE_SOFTMAX, True),
     ("ties_uniform", 2500, 8, 4, 700, 100, SAMPLE_UNIFORM, True),
     ("tiny", 5, 1, 1, 3, 1, SAMPLE_SOFTMAX, False),
-    # long heads (keys staged in LDS up to about 32k tokens), ties, extreme budgets
+    # long heads (keys held in registers up to 32k tokens), ties, extreme budgets
     ("long_softmax", 20000, 128, 128, 4000, 2000, SAMPLE_SOFTMAX, False),
     ("long_proportional", 9001, 40, 20, 1800, 600, SAMPLE_PROPORTIONAL, False),
     ("long_uniform", 12288, 64, 64, 2457, 1228, SAMPLE_UNIFORM, False),
