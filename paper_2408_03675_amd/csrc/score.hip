@@ -14,14 +14,15 @@
 //           Each key is owned by one wave: no atomics on F, so results are
 //           bit-reproducible.
 //
-// The kernel streams K straight from HBM into registers: each wave owns a
-// contiguous quarter of the chunk's keys and all proxies of the current proxy
-// group, so a K tile is used by exactly one wave and never staged in LDS.
-// Tiles of 16 keys are fetched with 16-byte non-temporal buffer loads a few
-// tiles ahead of the MFMAs that consume them (a register ring), which streams
-// at close to the HBM rate.  Pass 2 reads K a second time; a memory-side cache
-// does not serve that re-read faster than HBM on this part, so K crosses HBM
-// twice and the kernel is bound by 2 x |K| / HBM bandwidth.
+// The kernel streams K from HBM through a small LDS ring per wave: the
+// chunk's 16-key tiles are dealt round-robin to the block's waves, and each
+// wave works on its own tiles with all proxies of the current proxy group, so
+// a K tile is used by exactly one wave and the waves of a block read
+// neighbouring pieces of K at any moment.  Tiles are fetched by non-temporal
+// buffer loads that write the wave's LDS slots directly, several tiles ahead
+// of the MFMAs that consume them.  Pass 2 reads K a second time; a
+// memory-side cache does not serve that re-read faster than HBM on this part,
+// so K crosses HBM twice and the kernel is bound by 2 x |K| / HBM bandwidth.
 //
 // Work-groups take items from a queue counter in a fixed order: the pass-1
 // items of head group g + lag come before the pass-2 items of head group g,
@@ -356,9 +357,12 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     const T* qb = q + b * a.qs[0] + h * a.qs[1];
     const T* kb = k + b * a.ks[0] + h * a.ks[1];
     const int TPW = s.tpw;  // multiple of kUnroll, at most TPWMAX
-    const int keys_per_wave = TPW * 16;
     const int chunk_key0 = it.chunk * s.chunk_keys;
-    const int key_base = chunk_key0 + wave * keys_per_wave;
+    // The chunk's 16-key tiles are dealt round-robin to the waves: tile t of
+    // this wave holds keys tile_key(t) .. tile_key(t) + 15, so the waves of a
+    // block stream neighbouring 4 KB pieces of K at any moment (better DRAM
+    // page locality than one contiguous range per wave).
+    auto tile_key = [&](int t) -> int { return chunk_key0 + (t * kScoreWaves + wave) * 16; };
     const bool beyond = chunk_key0 > a.p_last;  // no proxy sees these keys
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<T*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + (uint32_t)(D * sizeof(T))),
@@ -373,7 +377,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     // beyond the descriptor and reads zeros without touching memory), so
     // every wait count is static.
     auto tile_byte = [&](int t) -> uint32_t {
-      return t < TPW ? (uint32_t)(key_base + 16 * t) * row_bytes : kOutOfRange;
+      return t < TPW ? (uint32_t)tile_key(t) * row_bytes : kOutOfRange;
     };
     auto slot = [&](auto u_c) -> unsigned char* {
       constexpr int u = decltype(u_c)::value % kDepth;
@@ -452,7 +456,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
           sm[pb] = 0.f;
         }
         auto mfma1 = [&](int t, const frag_t (&kf)[kS], auto& acc, auto p0_c, auto n_c) {
-          if (key_base + t * 16 > last) return;  // no proxy of the group sees this tile
+          if (tile_key(t) > last) return;  // no proxy of the group sees this tile
           tile_logits<M, PB, decltype(p0_c)::value, decltype(n_c)::value, true>(kf, qf, acc);
         };
         // VALU work of one tile; FULL tiles (every key visible to every proxy
@@ -460,7 +464,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         auto valu1_body = [&](int t, const auto& acc, auto p0_c, auto n_c, auto full_c) {
           constexpr int P0 = decltype(p0_c)::value, N = decltype(n_c)::value;
           constexpr bool FULL = decltype(full_c)::value;
-          const int key0 = key_base + t * 16;
+          const int key0 = tile_key(t);
           const int* pos_l = pos_g + opaque(r16);
 #pragma unroll
           for (int pb = P0; pb < P0 + N; ++pb) {
@@ -488,7 +492,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
           }
         };
         auto valu1 = [&](int t, const auto& acc, auto, auto p0_c, auto n_c) {
-          const int key0 = key_base + t * 16;
+          const int key0 = tile_key(t);
           if (key0 > last) return;
           if (key0 + 15 <= first) valu1_body(t, acc, p0_c, n_c, std::true_type{});
           else valu1_body(t, acc, p0_c, n_c, std::false_type{});
@@ -511,7 +515,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
 #pragma unroll
             for (int pb = 0; pb < PB; ++pb) sm[pb] = 0.f;
             for (int t = 0; t < TPW; ++t) {
-              const int key0 = key_base + t * 16;
+              const int key0 = tile_key(t);
               if (key0 > last) break;
               frag_t kf[kS];
               M::load_k(rsrc, voff + (uint32_t)key0 * row_bytes, kf);  // direct loads: rare path
@@ -634,7 +638,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         // wave's own LDS row; same-wave LDS accesses are ordered).
         float cs4[4];
         auto mfma2 = [&](int t, const frag_t (&kf)[kS], auto& acc, auto p0_c, auto n_c) {
-          if (key_base + t * 16 > last) return;
+          if (tile_key(t) > last) return;
           tile_logits<M, PB, decltype(p0_c)::value, decltype(n_c)::value, false>(kf, qf, acc);
         };
         // This lane's share of its key's column sum over blocks [P0, P0 + N);
@@ -663,7 +667,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         auto valu2 = [&](int t, const auto& acc, auto u_c, auto p0_c, auto n_c) {
           constexpr int u = decltype(u_c)::value;
           constexpr int P0 = decltype(p0_c)::value, N = decltype(n_c)::value;
-          const int key0 = key_base + t * 16;
+          const int key0 = tile_key(t);
           float cs = P0 == 0 ? 0.f : cs4[u % 4];
           if (key0 <= last) {
             if (key0 + 15 <= first) cs += valu2_body(key0, acc, p0_c, n_c, std::true_type{});
@@ -681,7 +685,8 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       __syncthreads();
       float* F = s.scores + (int64_t)bh * a.L;
       for (int idx = threadIdx.x; idx < s.chunk_keys; idx += kScoreThreads) {
-        const int kk = idx / keys_per_wave, j = idx % keys_per_wave;
+        const int tile = idx >> 4;  // the chunk's tile: wave tile % kScoreWaves, its tile tile / kScoreWaves
+        const int kk = tile % kScoreWaves, j = (tile / kScoreWaves) * 16 + (idx & 15);
         const int key = chunk_key0 + idx;
         if (key < a.L) F[key] = col_lds[kk][j];
       }
