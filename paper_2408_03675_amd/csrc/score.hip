@@ -650,9 +650,12 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
           const float* lse_l = lse_g + o;
           const int* pos_l = pos_g + o;
           float cs = 0.f;
+          f32x4 lrs[N];
+#pragma unroll
+          for (int pb = P0; pb < P0 + N; ++pb) lrs[pb - P0] = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
 #pragma unroll
           for (int pb = P0; pb < P0 + N; ++pb) {
-            const f32x4 lr = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
+            const f32x4 lr = lrs[pb - P0];
             float x[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb - P0][e], c2, -lr[e]));
