@@ -1,41 +1,36 @@
 // Cache update K0, V0 <- K_S, V_S (NaCl Section 3, encoding-phase eviction):
-// a row gather.  Each thread moves 16-byte vectors; the lanes covering one
-// row read it contiguously and the output rows are written contiguously, so
-// both sides are coalesced.  Rows are bit copies.
+// a row gather.  One thread moves one 16-byte vector: the lanes covering a
+// row read it contiguously and write it to a contiguous output row, so both
+// sides are coalesced.  K and V rows go to separate blocks (blockIdx.z), and
+// with no loop every thread's load is in flight from its first instruction;
+// many small blocks keep the whole chip issuing.  Rows are bit copies.
 
 #include "device_common.h"
 #include "internal.h"
 
 namespace nacl {
 
-constexpr int kCompactThreads = 256;
-constexpr int kCompactRowsPerBlock = 64;
+constexpr int kCompactThreads = 512;
 
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(CompactLaunch a) {
   const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
   const int vpr = a.row_vecs;
-  const int rows_per_pass = kCompactThreads / vpr;
+  const int r = blockIdx.x * (kCompactThreads / vpr) + (int)threadIdx.x / vpr;
+  if (r >= a.C) return;
   const int vec = threadIdx.x % vpr;
-  const int r_begin = blockIdx.x * kCompactRowsPerBlock;
-  const int r_end = min(r_begin + kCompactRowsPerBlock, a.C);
-  const u32x4* k = static_cast<const u32x4*>(a.k) + b * a.ks[0] + h * a.ks[1] + vec;
-  const u32x4* v = static_cast<const u32x4*>(a.v) + b * a.vs[0] + h * a.vs[1] + vec;
-  const int32_t* keep = a.keep + (int64_t)bh * a.C;
-  u32x4* ko = static_cast<u32x4*>(a.k_out) + (int64_t)bh * a.C * vpr + vec;
-  u32x4* vo = static_cast<u32x4*>(a.v_out) + (int64_t)bh * a.C * vpr + vec;
-#pragma unroll 4
-  for (int r = r_begin + (int)threadIdx.x / vpr; r < r_end; r += rows_per_pass) {
-    const int64_t j = keep[r];
-    const u32x4 kv = __builtin_nontemporal_load(k + j * a.ks[2]);
-    const u32x4 vv = __builtin_nontemporal_load(v + j * a.vs[2]);
-    __builtin_nontemporal_store(kv, ko + (int64_t)r * vpr);
-    __builtin_nontemporal_store(vv, vo + (int64_t)r * vpr);
-  }
+  const bool is_v = blockIdx.z != 0;
+  const int64_t* st = is_v ? a.vs : a.ks;
+  const int64_t j = a.keep[(int64_t)bh * a.C + r];
+  const u32x4* src = static_cast<const u32x4*>(is_v ? a.v : a.k) + b * st[0] + h * st[1] + j * st[2] + vec;
+  u32x4* dst = static_cast<u32x4*>(is_v ? a.v_out : a.k_out) + ((int64_t)bh * a.C + r) * vpr + vec;
+  __builtin_nontemporal_store(__builtin_nontemporal_load(src), dst);
 }
 
 hipError_t launch_compact(const CompactLaunch& a, hipStream_t stream) {
   if (a.C == 0) return hipSuccess;
-  dim3 grid((a.C + kCompactRowsPerBlock - 1) / kCompactRowsPerBlock, a.B * a.H);
+  if (a.row_vecs <= 0 || kCompactThreads % a.row_vecs != 0) return hipErrorInvalidValue;
+  const int rows_per_block = kCompactThreads / a.row_vecs;
+  dim3 grid((a.C + rows_per_block - 1) / rows_per_block, a.B * a.H, 2);
   hipLaunchKernelGGL(compact_kernel, grid, dim3(kCompactThreads), 0, stream, a);
   return hipGetLastError();
 }
