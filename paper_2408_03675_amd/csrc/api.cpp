@@ -160,8 +160,17 @@ int heads_per_group(int BH, int n_chunks, int target_items) {
   return best;
 }
 
+// Gumbel keys for the selection that follows, drawn by the score kernel
+// (inside nacl_evict only).
+struct KeyDraw {
+  bool on = false;
+  int32_t sampling = 0;
+  uint64_t seed = 0;
+  uint32_t layer = 0;
+};
+
 int run_score(const nacl_problem* p, const void* q, const void* k, const float* lse, float* scores,
-              char* ws, const Layout& l, const int* pos_dev, hipStream_t stream) {
+              char* ws, const Layout& l, const int* pos_dev, hipStream_t stream, const KeyDraw& kd = KeyDraw{}) {
   nacl::ScoreLaunch s{};
   s.args.B = p->B;
   s.args.H = p->H;
@@ -210,6 +219,11 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   sc.lse_in = lse;
   sc.lse_mul = 1.4426950408889634f;
   sc.scores = scores;
+  sc.gkeys = kd.on ? reinterpret_cast<uint32_t*>(ws + l.keys) : nullptr;
+  sc.g_mode = kd.sampling;
+  sc.g_k0 = (uint32_t)(kd.seed & 0xFFFFFFFFu);
+  sc.g_k1 = (uint32_t)(kd.seed >> 32);
+  sc.g_layer = kd.layer;
   s.n_counter_words = kCounterHeader + BH;
   hipError_t e = nacl::launch_score(s, stream);
   if (e != hipSuccess) return hip_fail(e, "score kernel");
@@ -218,7 +232,7 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
 
 int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr, int32_t sampling,
                uint64_t seed, uint32_t layer, int32_t* keep, char* ws, const Layout& l,
-               const int* pos_dev, hipStream_t stream) {
+               const int* pos_dev, hipStream_t stream, bool keys_ready = false) {
   if (C == 0) return NACL_OK;
   nacl::SelectLaunch s{};
   s.B = p->B;
@@ -236,6 +250,7 @@ int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr
   s.scores = scores;
   s.keys2 = reinterpret_cast<uint32_t*>(ws + l.keys);
   s.keep = keep;
+  s.keys_ready = keys_ready ? 1 : 0;
   hipError_t e = nacl::launch_select(s, stream);
   if (e != hipSuccess) return hip_fail(e, "select kernels");
   return NACL_OK;
@@ -355,8 +370,15 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
   char* w = static_cast<char*>(ws);
   const int* pos_dev = nullptr;
   if ((st = stage_positions(p, w, l, s, &pos_dev))) return st;
-  if ((st = run_score(p, q, k, nullptr, scores, w, l, pos_dev, s))) return st;
-  if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s))) return st;
+  // The column reduction also draws the Gumbel keys (the selection's key
+  // kernel is then skipped); the keys are the same bits either way.
+  KeyDraw kd;
+  kd.on = C > 0 && Cr > 0;
+  kd.sampling = sampling;
+  kd.seed = seed;
+  kd.layer = layer;
+  if ((st = run_score(p, q, k, nullptr, scores, w, l, pos_dev, s, kd))) return st;
+  if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s, kd.on))) return st;
   return run_compact(p, k, v, keep_idx, C, k_out, v_out, s);
 }
 

@@ -58,6 +58,12 @@ struct ScoreSched {
   const float* lse_in;   // caller's log-sum-exp when lse_given
   float lse_mul;         // log2(e) for a natural log-sum-exp
   float* scores;         // [B*H, L]
+  // Gumbel keys drawn by the column reduction for the selection that
+  // follows (nullptr: none): mode and Philox key and layer as in the
+  // selection.
+  uint32_t* gkeys;       // [B*H, L]
+  int g_mode;
+  uint32_t g_k0, g_k1, g_layer;
 };
 
 struct ScoreLaunch {
@@ -79,6 +85,7 @@ struct SelectLaunch {
   const float* scores;   // [B*H, L]
   uint32_t* keys2;       // workspace [B*H, L]
   int32_t* keep;         // [B*H, C]
+  int keys_ready;        // 1: keys2 already holds the Gumbel keys (drawn by the score kernel)
 };
 
 hipError_t launch_select(const SelectLaunch& L, hipStream_t stream);

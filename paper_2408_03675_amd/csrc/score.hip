@@ -51,6 +51,7 @@
 #include <type_traits>
 
 #include "device_common.h"
+#include "gumbel.h"
 #include "internal.h"
 
 namespace nacl {
@@ -364,6 +365,23 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     // page locality than one contiguous range per wave).
     auto tile_key = [&](int t) -> int { return chunk_key0 + (t * kScoreWaves + wave) * 16; };
     const bool beyond = chunk_key0 > a.p_last;  // no proxy sees these keys
+    // Inside a whole eviction the column reduction also draws the chunk's
+    // Gumbel keys for the selection that follows, from the chunk's scores
+    // f_of(idx) (the values just written to F): one Philox block of four
+    // keys per thread and step.
+    auto chunk_gumbel_keys = [&](auto&& f_of) {
+      uint32_t* gk = s.gkeys + (int64_t)bh * a.L;
+      for (int q4 = 4 * (int)threadIdx.x; q4 < s.chunk_keys; q4 += 4 * kScoreThreads) {
+        const int j0 = chunk_key0 + q4;
+        if (j0 >= a.L) break;
+        const int n = min(4, a.L - j0);
+        float fv[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int e = 0; e < n; ++e) fv[e] = f_of(q4 + e);
+        uint32_t kv[4];
+        gumbel_block_keys(s.g_mode, j0, n, b, h, s.g_layer, s.g_k0, s.g_k1, fv, kv);
+        for (int e = 0; e < n; ++e) gk[j0 + e] = kv[e];
+      }
+    };
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<T*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + (uint32_t)(D * sizeof(T))),
         kBufferRsrcWord3);
@@ -606,6 +624,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       float* F = s.scores + (int64_t)bh * a.L;
       const int end = min(chunk_key0 + s.chunk_keys, a.L);
       for (int j = chunk_key0 + threadIdx.x; j < end; j += kScoreThreads) F[j] = 0.f;
+      if (s.gkeys) chunk_gumbel_keys([](int) { return 0.f; });
     } else {
       // ---------------- pass 2: column sums of exp2(logit - LSE) ----------
       if (!s.lse_given) {
@@ -687,12 +706,17 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
       }
       __syncthreads();
       float* F = s.scores + (int64_t)bh * a.L;
+      // Key chunk_key0 + idx sits in tile idx / 16 of the chunk: wave
+      // (idx / 16) % kScoreWaves, that wave's tile (idx / 16) / kScoreWaves.
+      auto col_of = [&](int idx) -> float {
+        const int tile = idx >> 4;
+        return col_lds[tile % kScoreWaves][(tile / kScoreWaves) * 16 + (idx & 15)];
+      };
       for (int idx = threadIdx.x; idx < s.chunk_keys; idx += kScoreThreads) {
-        const int tile = idx >> 4;  // the chunk's tile: wave tile % kScoreWaves, its tile tile / kScoreWaves
-        const int kk = tile % kScoreWaves, j = (tile / kScoreWaves) * 16 + (idx & 15);
         const int key = chunk_key0 + idx;
-        if (key < a.L) F[key] = col_lds[kk][j];
+        if (key < a.L) F[key] = col_of(idx);
       }
+      if (s.gkeys) chunk_gumbel_keys(col_of);
     }
   }
 }

@@ -18,6 +18,7 @@
 
 #include "device_common.h"
 #include "internal.h"
+#include "gumbel.h"
 #include "philox.h"
 
 namespace nacl {
@@ -25,61 +26,10 @@ namespace nacl {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
 
-// ln(x) in binary64 for x >= 0 (ln 0 = -inf, ln inf = inf), to within a
-// few units in the last place: x = m 2^e with m in [sqrt(1/2), sqrt(2)),
-// ln m = 2 atanh(s) with s = (m - 1) / (m + 1), |s| < 0.172, summed as the
-// odd series 2 s (1 + s^2/3 + s^4/5 + ... + s^20/21) (the next term is
-// below 2^-59 relative), and e ln 2 added in two parts (ln 2 rounded to
-// binary64 and the rest).  The quotient takes a hardware reciprocal, two
-// Newton steps and one residual correction.  The keys are rounded to
-// binary32 afterwards, so a few binary64 units never matter except for a
-// key within that distance of a binary32 rounding boundary.
-__device__ __forceinline__ double ln_f64(double x) {
-  constexpr double kLn2 = 0.6931471805599453094172321;         // rounded to binary64
-  constexpr double kLn2Rest = 2.319046813846299558e-17;        // ln 2 - kLn2
-  constexpr double kSqrtHalf = 0.70710678118654752440;
-  double m = __builtin_amdgcn_frexp_mant(x);                   // [1/2, 1)
-  int e = __builtin_amdgcn_frexp_exp(x);
-  if (m < kSqrtHalf) {
-    m *= 2.0;
-    --e;
-  }
-  const double f = m - 1.0;                                    // exact
-  const double d = f + 2.0;
-  double r = __builtin_amdgcn_rcp(d);
-  r = fma(r, fma(-d, r, 1.0), r);
-  r = fma(r, fma(-d, r, 1.0), r);
-  double s = f * r;
-  s = fma(fma(-s, d, f), r, s);
-  const double z = s * s;
-  double q = 1.0 / 21;
-  q = fma(q, z, 1.0 / 19);
-  q = fma(q, z, 1.0 / 17);
-  q = fma(q, z, 1.0 / 15);
-  q = fma(q, z, 1.0 / 13);
-  q = fma(q, z, 1.0 / 11);
-  q = fma(q, z, 1.0 / 9);
-  q = fma(q, z, 1.0 / 7);
-  q = fma(q, z, 1.0 / 5);
-  q = fma(q, z, 1.0 / 3);
-  const double s2 = 2.0 * s;
-  const double lnm = fma(s2 * z, q, s2);
-  const double ed = (double)e;
-  const double p = ed * kLn2;
-  const double perr = fma(ed, kLn2, -p);                       // exact rounding error of p
-  const double res = p + (lnm + fma(ed, kLn2Rest, perr));
-  if (x == 0.0) return -INFINITY;
-  if (x == INFINITY) return INFINITY;
-  return res;
-}
-
-// Gumbel keys of every token: key = binary32(logw + g) with
-// g = -ln(-ln u) in binary64, u = (word + 1/2) / 2^32, word = Philox4x32-10
-// output j mod 4 at counter (j / 4, h, b, layer) under key = seed.
-// MODE selects the log-weight: 0 = F (Softmax(F)), 1 = ln F (weights F),
-// 2 = none (uniform).  One kernel per mode keeps each straight-line.  One
-// thread per Philox block, i.e. four consecutive tokens: 16-byte loads and
-// stores when the rows allow (vec), the block evaluated once.
+// Gumbel keys of every token (gumbel_order_key<MODE>), for a selection run
+// on its own.  One kernel per mode keeps each straight-line.  One thread per
+// Philox block, i.e. four consecutive tokens: 16-byte loads and stores when
+// the rows allow (vec), the block evaluated once.
 template <int MODE>
 __global__ __launch_bounds__(256) void gumbel_keys_kernel(const float* __restrict__ F, int H, int L,
                                                           uint32_t k0, uint32_t k1, uint32_t layer, int vec,
@@ -107,14 +57,7 @@ __global__ __launch_bounds__(256) void gumbel_keys_kernel(const float* __restric
   const uint32_t word[4] = {w.x, w.y, w.z, w.w};
   uint32_t kv[4];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const double u = ((double)word[e] + 0.5) * 0x1p-32;
-    const double g = -ln_f64(-ln_f64(u));
-    double key = g;
-    if constexpr (MODE == 0) key = (double)fv[e] + g;
-    if constexpr (MODE == 1) key = ln_f64((double)fv[e]) + g;
-    kv[e] = float_order_key((float)key);
-  }
+  for (int e = 0; e < 4; ++e) kv[e] = gumbel_order_key<MODE>(fv[e], word[e]);
   if (vec) {
     *reinterpret_cast<uint4*>(out) = uint4{kv[0], kv[1], kv[2], kv[3]};
   } else {
@@ -556,7 +499,7 @@ size_t select_lds_bytes(int L) {
 
 hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
   const int BH = a.B * a.H;
-  if (a.Cr > 0) {
+  if (a.Cr > 0 && !a.keys_ready) {
     dim3 gk((a.L + 1023) / 1024, BH);
     const uint32_t k0 = (uint32_t)(a.seed & 0xFFFFFFFFu), k1 = (uint32_t)(a.seed >> 32);
     // 16-byte rows: every row start 16-byte aligned (the workspace always is).

@@ -262,3 +262,26 @@ def test_evict_is_deterministic():
         assert torch.equal(x, y)
     c = nacl.evict(prob, q, k, v, w.C, w.Cr, 0, 7, 4, ws=ws)
     assert not torch.equal(a[1], c[1])
+
+
+@pytest.mark.parametrize("mode", [SAMPLE_SOFTMAX, SAMPLE_PROPORTIONAL, SAMPLE_UNIFORM])
+@pytest.mark.parametrize("where", ["end", "early"])
+def test_evict_draws_the_same_keys_as_select(mode, where):
+    """nacl_evict draws the Gumbel keys inside the column reduction (skipping
+    the selection's key kernel); its keep set must equal that of nacl_select
+    run on the same scores, which draws every key in its own kernel.  Proxies
+    at the end, or early so that whole chunks lie past the last proxy (scores
+    0, keys drawn on the zero path); L not a multiple of 4; every non-protected
+    slot random, so every key's value matters."""
+    B, H, L, D = 2, 3, 9001, 128
+    pos = list(range(L - 40, L)) if where == "end" else list(range(300, 340))
+    _say("evict keys", mode, where)
+    w = custom("keys", B, H, L, D, len(pos), dtype="bf16", data_seed=61)
+    q, k, v = make_layer(w, 0, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, pos)
+    C = 1800
+    for Cr in (C - len(pos), 700):
+        F, keep, _, _ = nacl.evict(prob, q, k, v, C, Cr, mode, 11, 2, ws=nacl.workspace(prob))
+        keep2 = nacl.select(prob, F, C, Cr, mode, 11, 2, ws=nacl.workspace(prob))
+        torch.cuda.synchronize()
+        assert torch.equal(keep, keep2), (mode, where, Cr)
