@@ -33,8 +33,8 @@ F32_PEAK_TFLOPS = 157.3        # dense fp32 MFMA
 # (FETCH_SIZE, then WRITE_SIZE) scaled by the same counters on a plain copy of
 # known size; summarised under profiles/.  It is reported only while the
 # kernel source hashes to the value it was measured on.
-MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_kernel", "bytes_per_launch": 2231705360,
-                    "source_sha": "e0e698fa60cbda7d"}
+MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_split_kernel", "bytes_per_launch": 2215319797,
+                    "source_sha": "f88065000521ffef"}
 
 
 def _source_sha(rel):
@@ -144,8 +144,11 @@ def main():
 
     # Per-stage durations through the public entry points, timed with events
     # on the launch stream.  nacl_score = score_init_kernel (zeroes the work
-    # queue counters, ~5 us) + score_kernel; nacl_select = gumbel_keys_kernel
-    # + select_kernel; nacl_compact = compact_kernel.
+    # queue counters, ~5 us) + the score kernel (score_split_kernel for bf16,
+    # D = 128 and at least 128 proxies, else score_kernel); nacl_select =
+    # gumbel_keys_kernel + select_kernel_regs (select_kernel_global past 32k
+    # tokens); nacl_compact = compact_kernel.  Inside nacl_evict the score
+    # kernel also draws the Gumbel keys and the key kernel is skipped.
     def timed(fn):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         torch.cuda.synchronize()
@@ -205,13 +208,15 @@ def main():
         stages["score_pass2_only_us"] = round(t_pass2, 2)
     log(f"[bench] stages {json.dumps(stages)}")
 
-    # Dominant kernel: score_kernel.  Its roofline is HBM (algorithmic
+    # Dominant kernel: the score kernel.  Its roofline is HBM (algorithmic
     # intensity P flop/byte, below the bf16 ridge of ~312): algorithmic bytes
     # = K read once + proxy rows of Q + F written, per launch (one layer).
-    dom = {"kernel": "score_kernel", "bound": "hbm", "us": t_score,
+    split = w.dtype == "bf16" and w.D == 128 and w.P >= 128
+    dom = {"kernel": "score_split_kernel" if split else "score_kernel", "bound": "hbm", "us": t_score,
            "achieved": ab["score"] / (t_score * 1e3), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     traffic = None
     if MEASURED_TRAFFIC and MEASURED_TRAFFIC.get("workload") == w.name and \
+            MEASURED_TRAFFIC.get("kernel") == dom["kernel"] and \
             MEASURED_TRAFFIC.get("source_sha") == _source_sha("paper_2408_03675_amd/csrc/score.hip"):
         traffic = MEASURED_TRAFFIC["bytes_per_launch"]
     roofline = {"bound": dom["bound"], "achieved": round(dom["achieved"], 1), "peak": dom["peak"],

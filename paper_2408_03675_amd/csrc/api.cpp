@@ -205,8 +205,12 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
     if (items >= 4 * 2 * (int64_t)cus) sc.tpw = t;
   }
   sc.chunk_keys = sc.tpw * nacl::kScoreWaves * 16;
+  // The proxy-split kernel takes fixed items of kSplitChunkKeys keys.
+  if (nacl::score_uses_split(p->dtype, p->D, p->P)) sc.chunk_keys = nacl::kSplitChunkKeys;
   sc.n_chunks = (p->L + sc.chunk_keys - 1) / sc.chunk_keys;  // <= l.n_chunks
-  sc.heads_per_group = heads_per_group(BH, sc.n_chunks, NACL_SCORE_GROUP_ITEMS_PER_CU * cus);
+  const int group_items = nacl::score_uses_split(p->dtype, p->D, p->P) ? NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
+                                                                       : NACL_SCORE_GROUP_ITEMS_PER_CU;
+  sc.heads_per_group = heads_per_group(BH, sc.n_chunks, group_items * cus);
   sc.n_groups = BH / sc.heads_per_group;
   sc.lag = std::min(NACL_SCORE_LAG, sc.n_groups);
   sc.total_items = passes * BH * sc.n_chunks;

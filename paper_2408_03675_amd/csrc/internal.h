@@ -21,6 +21,9 @@ namespace nacl {
 #ifndef NACL_SCORE_GROUP_ITEMS_PER_CU
 #define NACL_SCORE_GROUP_ITEMS_PER_CU 2
 #endif
+#ifndef NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
+#define NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU 4
+#endif
 #ifndef NACL_SCORE_LAG
 #define NACL_SCORE_LAG 1
 #endif
@@ -30,7 +33,16 @@ constexpr int kScoreTpwMin = 32;
 constexpr int kScoreTpwMax = NACL_SCORE_TPW_MAX;
 constexpr int kScoreWavesPerSimd = NACL_SCORE_WAVES;
 constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter of the item's keys
-constexpr int kScoreMinChunkKeys = kScoreTpwMin * kScoreWaves * 16;
+// Proxy-split variant (bf16, D = 128, at least 128 proxies): the waves of a
+// block share one ring of K tiles and split each group of 128 proxies, so an
+// item is kSplitChunkKeys keys.
+#ifndef NACL_SCORE_SPLIT
+#define NACL_SCORE_SPLIT 1
+#endif
+constexpr int kSplitChunkKeys = 1024;
+inline bool score_uses_split(int dtype, int D, int P) { return NACL_SCORE_SPLIT && dtype == 1 && D == 128 && P >= 128; }
+// The workspace is sized for the shortest item of either kernel.
+constexpr int kScoreMinChunkKeys = std::min(kScoreTpwMin * kScoreWaves * 16, kSplitChunkKeys);
 
 struct ScoreArgs {
   int B, H, L, P;

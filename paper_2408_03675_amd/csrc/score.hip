@@ -24,6 +24,11 @@
 // memory-side cache does not serve that re-read faster than HBM on this part,
 // so K crosses HBM twice and the kernel is bound by 2 x |K| / HBM bandwidth.
 //
+// For bf16 inputs with D = 128 and at least 128 proxies, score_split_kernel
+// (below) replaces this layout: the waves of a block share the tile ring and
+// split the proxy group instead, which frees registers for a third block per
+// CU.  Everything else (queue, passes, merge, reproducibility) is the same.
+//
 // Work-groups take items from a queue counter in a fixed order: the pass-1
 // items of head group g + lag come before the pass-2 items of head group g,
 // so a pass-2 item rarely finds its head's log-sum-exp unpublished.  A
@@ -727,6 +732,394 @@ __global__ void score_init_kernel(uint32_t* words, int n) {
 }
 
 // ---------------------------------------------------------------------------
+// Proxy-split variant: bf16, D = 128, groups of 128 proxies.  The four waves
+// of a block share one LDS ring of K tiles and split the proxy group: wave w
+// takes proxies [32w, 32w + 32) of every tile, so it holds a quarter of the
+// group's Q fragments and three blocks fit on a CU (more waves to hide the
+// MFMA, exponential and LDS latencies behind the K stream).  Each wave issues
+// one of a tile's four DMA instructions; one block barrier per tile makes the
+// whole tile visible and guarantees that the slot refilled next was read by
+// every wave one step earlier.  An item is kSplitChunkKeys keys; pass 1 needs
+// no merge across waves (each wave owns its proxies' sums over all the
+// item's keys), pass 2 adds the four waves' partial column sums.
+constexpr int kSplitDepth = 8;                               // ring slots per block
+constexpr int kSplitTiles = kSplitChunkKeys / 16;            // tiles per item
+constexpr int kSplitWaveBlocks = 2;                          // proxy blocks of 16 per wave
+constexpr int kSplitGroup = 16 * kSplitWaveBlocks * kScoreWaves;  // 128 proxies
+static_assert(kSplitTiles % kSplitDepth == 0 && kSplitDepth % 4 == 0, "tiles per item vs ring");
+
+__device__ __forceinline__ void block_barrier() {
+  // A barrier without the fence of __syncthreads(): waits for no memory
+  // operation, so the DMA of later tiles stays in flight across it.
+  asm volatile("s_barrier" ::: "memory");
+}
+
+__global__ __launch_bounds__(kScoreThreads, 3) void score_split_kernel(const __bf16* __restrict__ q,
+                                                                       const __bf16* __restrict__ k,
+                                                                       ScoreArgs a, ScoreSched s) {
+  using T = __bf16;
+  constexpr int D = 128;
+  using M = Mma<T, D>;
+  using KS = KStage<T, D>;
+  using frag_t = typename M::frag_t;
+  constexpr int kS = M::kSteps;
+  constexpr int WB = kSplitWaveBlocks;
+  static_assert(KS::kInstr == kScoreWaves, "one DMA instruction per wave and tile");
+  __shared__ int item_s, last_s;
+  __shared__ int pos_g[kSplitGroup];
+  __shared__ float2 mrg[kScoreThreads];
+  __shared__ float col_lds[kScoreWaves][kSplitChunkKeys];
+  __shared__ __attribute__((aligned(16))) float lse_g[kSplitGroup];
+#define NACL_SSLOT(i) __shared__ __attribute__((aligned(16))) unsigned char sslot##i[KS::kTileBytes];
+  NACL_SSLOT(0) NACL_SSLOT(1) NACL_SSLOT(2) NACL_SSLOT(3) NACL_SSLOT(4) NACL_SSLOT(5) NACL_SSLOT(6) NACL_SSLOT(7)
+#undef NACL_SSLOT
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const float c2 = a.c2;
+  float* my_cols = col_lds[wave];
+  const uint32_t row_bytes = (uint32_t)(a.ks[2] * (int64_t)sizeof(T));
+  // This wave's DMA instruction of a tile: rows kRowsPerInstr * wave ...
+  uint32_t vo_all[KS::kInstr];
+  KS::offsets(row_bytes, lane, vo_all);
+  uint32_t vo = vo_all[0];
+#pragma unroll
+  for (int i = 1; i < KS::kInstr; ++i) vo = wave == i ? vo_all[i] : vo;
+  const uint32_t voff = (uint32_t)r16 * row_bytes + 16u * (uint32_t)g;  // direct fragment loads (exact path)
+  const int w0 = 16 * WB * wave;  // this wave's first proxy within the group
+
+  for (;;) {
+    __syncthreads();
+    if (threadIdx.x == 0) item_s = (int)atomicAdd(s.queue, 1u);
+    __syncthreads();
+    const int item = __builtin_amdgcn_readfirstlane(item_s);
+    if (item >= s.total_items) break;
+    const ItemRef it = decode_item(s, item);
+    const int bh = it.bh, b = bh / a.H, h = bh % a.H;
+    const T* qb = q + b * a.qs[0] + h * a.qs[1];
+    const T* kb = k + b * a.ks[0] + h * a.ks[1];
+    const int chunk_key0 = it.chunk * kSplitChunkKeys;
+    const bool beyond = chunk_key0 > a.p_last;
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + (uint32_t)(D * sizeof(T))),
+        kBufferRsrcWord3);
+    auto tile_byte = [&](int t) -> uint32_t {
+      return t < kSplitTiles ? (uint32_t)(chunk_key0 + 16 * t) * row_bytes : kOutOfRange;
+    };
+    auto slot = [&](auto u_c) -> unsigned char* {
+      constexpr int u = decltype(u_c)::value % kSplitDepth;
+      if constexpr (u == 0) return sslot0;
+      else if constexpr (u == 1) return sslot1;
+      else if constexpr (u == 2) return sslot2;
+      else if constexpr (u == 3) return sslot3;
+      else if constexpr (u == 4) return sslot4;
+      else if constexpr (u == 5) return sslot5;
+      else if constexpr (u == 6) return sslot6;
+      else return sslot7;
+    };
+    auto issue = [&](int t, unsigned char* dst) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(dst + wave * 1024), 16,
+                                               vo + tile_byte(t), 0, 0, kScoreKAux);
+    };
+    // Streams the item's tiles through the shared ring and calls
+    // tile_fn(t, kf, u_c) with tile t's fragments.  Step t: wait for this
+    // wave's part of tile t, barrier (every part landed; every wave is done
+    // with tile t - 1), refill tile t - 1's slot with tile t + kSplitDepth - 1,
+    // read tile t.  The DMA is unconditional (tiles past the item read
+    // nothing), so every wait count is static.
+    auto k_tiles = [&](auto&& tile_fn) {
+      static_for<kSplitDepth - 1>([&](auto u_c) { issue(decltype(u_c)::value, slot(u_c)); });
+#pragma unroll 1
+      for (int t = 0; t < kSplitTiles; t += kSplitDepth) {
+        static_for<kSplitDepth>([&](auto u_c) {
+          constexpr int u = decltype(u_c)::value;
+          const int tt = t + u;
+          asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kSplitDepth - 2) : "memory");
+          block_barrier();
+          issue(tt + kSplitDepth - 1, slot(std::integral_constant<int, u + kSplitDepth - 1>{}));
+          frag_t kf[kS];
+          KS::template frag<M>(slot(u_c), r16, g, kf);
+          tile_fn(tt, kf, u_c);
+        });
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    };
+    auto load_group = [&](int g0, int gn) {
+      __syncthreads();
+      for (int i = threadIdx.x; i < kSplitGroup; i += kScoreThreads) pos_g[i] = i < gn ? a.pos[g0 + i] : -1;
+      __syncthreads();
+    };
+    // This wave's Q fragments (zeros past the group's end) and the positions
+    // of its first and last proxy (no proxy: first = INT_MAX, last = -1).
+    auto load_wave_q = [&](int gn, frag_t (&qf)[WB][kS], int& first, int& last) {
+#pragma unroll
+      for (int pb = 0; pb < WB; ++pb) {
+        const int i = w0 + 16 * pb + r16;
+        if (i < gn) M::load(qb + (int64_t)pos_g[i] * a.qs[2], g, qf[pb]);
+        else M::zero(qf[pb]);
+      }
+      const int wn = min(max(gn - w0, 0), 16 * WB);
+      first = wn > 0 ? pos_g[w0] : 0x7FFFFFFF;
+      last = wn > 0 ? pos_g[w0 + wn - 1] : -1;
+    };
+    auto chunk_gumbel_keys = [&](auto&& f_of) {
+      uint32_t* gk = s.gkeys + (int64_t)bh * a.L;
+      for (int q4 = 4 * (int)threadIdx.x; q4 < kSplitChunkKeys; q4 += 4 * kScoreThreads) {
+        const int j0 = chunk_key0 + q4;
+        if (j0 >= a.L) break;
+        const int n = min(4, a.L - j0);
+        float fv[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int e = 0; e < n; ++e) fv[e] = f_of(q4 + e);
+        uint32_t kv[4];
+        gumbel_block_keys(s.g_mode, j0, n, b, h, s.g_layer, s.g_k0, s.g_k1, fv, kv);
+        for (int e = 0; e < n; ++e) gk[j0 + e] = kv[e];
+      }
+    };
+
+    if (it.kind == 1) {
+      // ---------------- pass 1: per-chunk (reference, sum) of every proxy row
+      float2* part = s.partials + ((int64_t)bh * s.n_chunks + it.chunk) * a.P;
+      if (beyond)
+        for (int i = threadIdx.x; i < a.P; i += kScoreThreads)
+          store_coherent(part + i, make_float2(-INFINITY, 0.f));
+      for (int g0 = 0; g0 < (beyond ? 0 : a.P); g0 += kSplitGroup) {
+        const int gn = min(kSplitGroup, a.P - g0);
+        load_group(g0, gn);
+        frag_t qf[WB][kS];
+        int first, last;
+        load_wave_q(gn, qf, first, last);
+        // Per proxy block: base-2 reference (the scaled maximum of the item's
+        // first tile, 0 if that tile shows the proxy nothing) and the running
+        // sum of exp2(logit * c2 - ref) over this lane's keys (visibility is a
+        // prefix of the keys: see the main kernel).
+        float ref[WB], sm[WB];
+#pragma unroll
+        for (int pb = 0; pb < WB; ++pb) {
+          ref[pb] = 0.f;
+          sm[pb] = 0.f;
+        }
+        auto body1 = [&](int t, const f32x4 (&acc)[WB], auto full_c) {
+          constexpr bool FULL = decltype(full_c)::value;
+          const int key0 = chunk_key0 + 16 * t;
+          const int* pos_l = pos_g + w0 + opaque(r16);
+#pragma unroll
+          for (int pb = 0; pb < WB; ++pb) {
+            bool vis[4];
+            if constexpr (!FULL) {
+              const int pi = pos_l[16 * pb];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) vis[e] = key0 + 4 * g + e <= pi;
+            }
+            if (t == 0) {
+              float mx = -INFINITY;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) mx = (FULL || vis[e]) ? fmaxf(mx, acc[pb][e]) : mx;
+              mx = max_over_groups(mx);
+              ref[pb] = mx != -INFINITY ? mx * c2 : 0.f;
+            }
+            float x[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb][e], c2, -ref[pb]));
+            if constexpr (!FULL) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = vis[e] ? x[e] : 0.f;
+            }
+            sm[pb] += (x[0] + x[1]) + (x[2] + x[3]);
+          }
+        };
+        k_tiles([&](int t, const frag_t (&kf)[kS], auto) {
+          const int key0 = chunk_key0 + 16 * t;
+          if (key0 > last) return;
+          f32x4 acc[WB];
+          tile_logits<M, WB, 0, WB, true>(kf, qf, acc);
+          if (key0 + 15 <= first) body1(t, acc, std::true_type{});
+          else body1(t, acc, std::false_type{});
+        });
+        bool bad = false;
+#pragma unroll
+        for (int pb = 0; pb < WB; ++pb) {
+          sm[pb] = sum_over_groups(sm[pb]);
+          bad |= !(sm[pb] <= 3.0e38f);
+        }
+        if (__builtin_amdgcn_ballot_w64(bad)) {
+          // Exact path (this wave only): the maximum over every visible key,
+          // then the sums, with direct loads.
+          float mx[WB];
+#pragma unroll
+          for (int pb = 0; pb < WB; ++pb) mx[pb] = -INFINITY;
+          for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+            for (int pb = 0; pb < WB; ++pb) sm[pb] = 0.f;
+            for (int t = 0; t < kSplitTiles; ++t) {
+              const int key0 = chunk_key0 + 16 * t;
+              if (key0 > last) break;
+              frag_t kf[kS];
+              M::load_k(rsrc, voff + (uint32_t)key0 * row_bytes, kf);
+              f32x4 acc[WB];
+              tile_logits<M, WB, 0, WB, true>(kf, qf, acc);
+#pragma unroll
+              for (int pb = 0; pb < WB; ++pb) {
+                const int pi = pos_g[w0 + 16 * pb + r16];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const bool v = key0 + 4 * g + e <= pi;
+                  if (pass == 0) mx[pb] = v ? fmaxf(mx[pb], acc[pb][e]) : mx[pb];
+                  else sm[pb] += v ? fast_exp2(fmaf(acc[pb][e], c2, -ref[pb])) : 0.f;
+                }
+              }
+            }
+            if (pass == 0) {
+#pragma unroll
+              for (int pb = 0; pb < WB; ++pb) {
+                mx[pb] = max_over_groups(mx[pb]);
+                ref[pb] = mx[pb] != -INFINITY ? mx[pb] * c2 : 0.f;
+              }
+            }
+          }
+#pragma unroll
+          for (int pb = 0; pb < WB; ++pb) sm[pb] = sum_over_groups(sm[pb]);
+        }
+        if (g == 0) {
+#pragma unroll
+          for (int pb = 0; pb < WB; ++pb) {
+            const int i = w0 + 16 * pb + r16;
+            if (i < gn)
+              store_coherent(part + g0 + i, sm[pb] > 0.f ? make_float2(ref[pb], sm[pb]) : make_float2(-INFINITY, 0.f));
+          }
+        }
+      }
+      // Publish the partials; the last chunk of the head merges them.
+      wait_stores();
+      __syncthreads();
+      if (threadIdx.x == 0) last_s = atomicAdd(&s.head_cnt[bh], 1u) == (unsigned)(s.n_chunks - 1);
+      __syncthreads();
+      if (last_s) {
+        const float2* hp = s.partials + (int64_t)bh * s.n_chunks * a.P;
+        const int split = a.P >= kScoreThreads ? 1 : kScoreThreads / a.P;
+        const int part_i = threadIdx.x / a.P;
+        constexpr int kBatch = 8;
+        for (int i0 = 0; i0 < a.P; i0 += kScoreThreads) {
+          const int i = i0 + (split == 1 ? (int)threadIdx.x : (int)threadIdx.x % a.P);
+          float mm = -INFINITY, ss = 0.f;
+          if (i < a.P && part_i < split) {
+            for (int c0 = part_i; c0 < s.n_chunks; c0 += kBatch * split) {
+              float2 v[kBatch];
+#pragma unroll
+              for (int u = 0; u < kBatch; ++u) {
+                const int c = c0 + u * split;
+                v[u] = c < s.n_chunks ? load_coherent(hp + (int64_t)c * a.P + i) : make_float2(-INFINITY, 0.f);
+              }
+#pragma unroll
+              for (int u = 0; u < kBatch; ++u) lse_merge(mm, ss, v[u].x, v[u].y);
+            }
+          }
+          if (split > 1) {
+            mrg[threadIdx.x] = make_float2(mm, ss);
+            __syncthreads();
+            if (part_i == 0 && i < a.P)
+              for (int pp = 1; pp < split; ++pp) {
+                const float2 r = mrg[threadIdx.x + pp * a.P];
+                lse_merge(mm, ss, r.x, r.y);
+              }
+          }
+          if (part_i == 0 && i < a.P) store_coherent(s.lse2 + (int64_t)bh * a.P + i, mm + __log2f(ss));
+        }
+        wait_stores();
+        __syncthreads();
+        if (threadIdx.x == 0) atomicAdd(&s.head_cnt[bh], 1u);
+      }
+    } else if (beyond) {
+      float* F = s.scores + (int64_t)bh * a.L;
+      const int end = min(chunk_key0 + kSplitChunkKeys, a.L);
+      for (int j = chunk_key0 + threadIdx.x; j < end; j += kScoreThreads) F[j] = 0.f;
+      if (s.gkeys) chunk_gumbel_keys([](int) { return 0.f; });
+    } else {
+      // ---------------- pass 2: column sums of exp2(logit - LSE) ----------
+      if (!s.lse_given) {
+        if (threadIdx.x == 0) {
+          uint32_t spins = 0;
+          while (load_coherent(&s.head_cnt[bh]) < (unsigned)(s.n_chunks + 1)) {
+            __builtin_amdgcn_s_sleep(2);
+            if (++spins > kSpinLimit) {
+              atomicOr(s.status, 1u);
+              break;
+            }
+          }
+        }
+        __syncthreads();
+      }
+      const float* lse = s.lse_given ? s.lse_in : s.lse2;
+      const float lse_mul = s.lse_given ? s.lse_mul : 1.0f;
+      for (int g0 = 0; g0 < a.P; g0 += kSplitGroup) {
+        const int gn = min(kSplitGroup, a.P - g0);
+        load_group(g0, gn);
+        frag_t qf[WB][kS];
+        int first, last;
+        load_wave_q(gn, qf, first, last);
+        for (int i = threadIdx.x; i < kSplitGroup; i += kScoreThreads)
+          lse_g[i] = i < gn ? load_coherent(lse + (int64_t)bh * a.P + g0 + i) * lse_mul : INFINITY;
+        __syncthreads();
+        // This lane's share of its key's column sum over the wave's proxies;
+        // FULL tiles carry no masking.
+        auto body2 = [&](int key0, const f32x4 (&acc)[WB], auto full_c) -> float {
+          constexpr bool FULL = decltype(full_c)::value;
+          const int o = w0 + opaque(4 * g);
+          const float* lse_l = lse_g + o;
+          const int* pos_l = pos_g + o;
+          f32x4 lrs[WB];
+#pragma unroll
+          for (int pb = 0; pb < WB; ++pb) lrs[pb] = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
+          float cs = 0.f;
+#pragma unroll
+          for (int pb = 0; pb < WB; ++pb) {
+            float x[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb][e], c2, -lrs[pb][e]));
+            if constexpr (!FULL) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = key0 + r16 <= pos_l[16 * pb + e] ? x[e] : 0.f;
+            }
+            cs += (x[0] + x[1]) + (x[2] + x[3]);
+          }
+          return cs;
+        };
+        // Partial column sums of the last four tiles; every fourth tile they
+        // are reduced across lane groups and lane group g stores tile t - 3 + g.
+        float cs4[4];
+        k_tiles([&](int t, const frag_t (&kf)[kS], auto u_c) {
+          constexpr int u = decltype(u_c)::value;
+          const int key0 = chunk_key0 + 16 * t;
+          float cs = 0.f;
+          if (key0 <= last) {
+            f32x4 acc[WB];
+            tile_logits<M, WB, 0, WB, false>(kf, qf, acc);
+            if (key0 + 15 <= first) cs = body2(key0, acc, std::true_type{});
+            else cs = body2(key0, acc, std::false_type{});
+          }
+          cs4[u % 4] = cs;
+          if constexpr (u % 4 == 3) {
+            const float z = colsum4(cs4[0], cs4[1], cs4[2], cs4[3]);
+            const int idx = (t - 3) * 16 + lane;
+            my_cols[idx] = (g0 == 0 ? 0.f : my_cols[idx]) + z;
+          }
+        });
+      }
+      __syncthreads();
+      float* F = s.scores + (int64_t)bh * a.L;
+      auto col_of = [&](int idx) -> float {
+        return ((col_lds[0][idx] + col_lds[1][idx]) + col_lds[2][idx]) + col_lds[3][idx];
+      };
+      for (int idx = threadIdx.x; idx < kSplitChunkKeys; idx += kScoreThreads) {
+        const int key = chunk_key0 + idx;
+        if (key < a.L) F[key] = col_of(idx);
+      }
+      if (s.gkeys) chunk_gumbel_keys(col_of);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host-side launchers.
 
 namespace {
@@ -760,7 +1153,29 @@ int proxy_blocks(int dtype, int D, int P) {
 
 }  // namespace
 
+hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
+  auto kern = score_split_kernel;
+  int per_cu = 0;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kScoreThreads, 0);
+  if (e != hipSuccess) return e;
+  int dev = 0, cus = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  const int grid = std::max(1, std::min(L.sched.total_items, std::max(1, per_cu) * cus));
+  const int init_blocks = std::max(1, std::min(64, (L.n_counter_words + 255) / 256));
+  hipLaunchKernelGGL(score_init_kernel, dim3(init_blocks), dim3(256), 0, stream, L.sched.queue,
+                     L.n_counter_words);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kScoreThreads), 0, stream, static_cast<const __bf16*>(L.q),
+                     static_cast<const __bf16*>(L.k), L.args, L.sched);
+  return hipGetLastError();
+}
+
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream) {
+  if (score_uses_split(L.dtype, L.D, L.args.P)) {
+    if (L.sched.chunk_keys != kSplitChunkKeys) return hipErrorInvalidValue;
+    return launch_score_split(L, stream);
+  }
   const int pb = proxy_blocks(L.dtype, L.D, L.args.P);
   if (L.dtype == 1) {
     if (L.D == 128) {
