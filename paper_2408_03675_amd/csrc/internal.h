@@ -22,7 +22,7 @@ namespace nacl {
 #define NACL_SCORE_GROUP_ITEMS_PER_CU 2
 #endif
 #ifndef NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
-#define NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU 4
+#define NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU 8
 #endif
 #ifndef NACL_SCORE_LAG
 #define NACL_SCORE_LAG 1
@@ -39,7 +39,10 @@ constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter o
 #ifndef NACL_SCORE_SPLIT
 #define NACL_SCORE_SPLIT 1
 #endif
-constexpr int kSplitChunkKeys = 1024;
+#ifndef NACL_SPLIT_CHUNK
+#define NACL_SPLIT_CHUNK 1024
+#endif
+constexpr int kSplitChunkKeys = NACL_SPLIT_CHUNK;
 inline bool score_uses_split(int dtype, int D, int P) { return NACL_SCORE_SPLIT && dtype == 1 && D == 128 && P >= 128; }
 // The workspace is sized for the shortest item of either kernel.
 constexpr int kScoreMinChunkKeys = std::min(kScoreTpwMin * kScoreWaves * 16, kSplitChunkKeys);

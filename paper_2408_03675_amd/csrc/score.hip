@@ -26,7 +26,7 @@
 //
 // For bf16 inputs with D = 128 and at least 128 proxies, score_split_kernel
 // (below) replaces this layout: the waves of a block share the tile ring and
-// split the proxy group instead, which frees registers for a third block per
+// split the proxy group instead, which frees registers for four blocks per
 // CU.  Everything else (queue, passes, merge, reproducibility) is the same.
 //
 // Work-groups take items from a queue counter in a fixed order: the pass-1
@@ -735,14 +735,20 @@ __global__ void score_init_kernel(uint32_t* words, int n) {
 // Proxy-split variant: bf16, D = 128, groups of 128 proxies.  The four waves
 // of a block share one LDS ring of K tiles and split the proxy group: wave w
 // takes proxies [32w, 32w + 32) of every tile, so it holds a quarter of the
-// group's Q fragments and three blocks fit on a CU (more waves to hide the
+// group's Q fragments and four blocks fit on a CU (more waves to hide the
 // MFMA, exponential and LDS latencies behind the K stream).  Each wave issues
 // one of a tile's four DMA instructions; one block barrier per tile makes the
 // whole tile visible and guarantees that the slot refilled next was read by
 // every wave one step earlier.  An item is kSplitChunkKeys keys; pass 1 needs
 // no merge across waves (each wave owns its proxies' sums over all the
 // item's keys), pass 2 adds the four waves' partial column sums.
-constexpr int kSplitDepth = 8;                               // ring slots per block
+#ifndef NACL_SPLIT_DEPTH
+#define NACL_SPLIT_DEPTH 4
+#endif
+#ifndef NACL_SPLIT_OCC
+#define NACL_SPLIT_OCC 4
+#endif
+constexpr int kSplitDepth = NACL_SPLIT_DEPTH;                // ring slots per block (at most 8)
 constexpr int kSplitTiles = kSplitChunkKeys / 16;            // tiles per item
 constexpr int kSplitWaveBlocks = 2;                          // proxy blocks of 16 per wave
 constexpr int kSplitGroup = 16 * kSplitWaveBlocks * kScoreWaves;  // 128 proxies
@@ -754,7 +760,7 @@ __device__ __forceinline__ void block_barrier() {
   asm volatile("s_barrier" ::: "memory");
 }
 
-__global__ __launch_bounds__(kScoreThreads, 3) void score_split_kernel(const __bf16* __restrict__ q,
+__global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_kernel(const __bf16* __restrict__ q,
                                                                        const __bf16* __restrict__ k,
                                                                        ScoreArgs a, ScoreSched s) {
   using T = __bf16;
