@@ -93,10 +93,12 @@ def test_score_strided_inputs():
     check_scores(F.cpu().numpy(), Fr, "strided")
 
 
-def test_score_with_caller_lse():
+@pytest.mark.parametrize("P", [40, 160])
+def test_score_with_caller_lse(P):
     """With the caller's log-sum-exp (Appendix A.7, Algorithm 2) only the
-    column reduction runs and gives the same scores."""
-    w = custom("lse", 1, 3, 1500, 128, 40, dtype="bf16", data_seed=3)
+    column reduction runs and gives the same scores (P = 160: the proxy-split
+    kernel, a full and a partial proxy group)."""
+    w = custom("lse", 1, 3, 1500, 128, P, dtype="bf16", data_seed=3)
     q, k, v = make_layer(w, 0, device="cuda")
     pos = w.proxy_pos
     prob = nacl.Problem.from_tensors(q, k, v, pos)
@@ -106,19 +108,20 @@ def test_score_with_caller_lse():
     check_scores(F.cpu().numpy(), Fr, "caller lse")
 
 
-def test_score_overflow_takes_exact_path():
+@pytest.mark.parametrize("P", [100, 160])
+def test_score_overflow_takes_exact_path(P):
     """Pass 1 sums exp2(logit - r) against the maximum r of the first tile of
-    each wave's key range; a later key far above r overflows fp32, and the
+    each item's key range; a later key far above r overflows fp32, and the
     kernel recomputes that range's sums against its exact maximum.  Here one
     key per head sits about 180 (natural-log units) above every other logit
     of its range, so the fast path overflows and the scores are dominated by
-    that key."""
+    that key (P = 160: the proxy-split kernel)."""
     B, H, L, D = 1, 2, 3000, 128
     g = torch.Generator(device="cuda").manual_seed(11)
     q = torch.randn((B, H, L, D), generator=g, device="cuda")
     k = torch.randn((B, H, L, D), generator=g, device="cuda")
-    pos = list(range(2900, 3000))
-    q[:, :, 2900:] += 2.0        # proxy rows with a positive mean
+    pos = list(range(L - P, L))
+    q[:, :, L - P:] += 2.0       # proxy rows with a positive mean
     k[:, 0, 1000] = 8.0          # head 0: a key inside a range, not in its first tile
     k[:, 1, 2500] = 8.0          # head 1: the same in another item
     q, k = q.to(torch.bfloat16), k.to(torch.bfloat16)
