@@ -22,7 +22,7 @@ namespace nacl {
 #define NACL_SCORE_GROUP_ITEMS_PER_CU 2
 #endif
 #ifndef NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
-#define NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU 8
+#define NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU 4
 #endif
 #ifndef NACL_SCORE_LAG
 #define NACL_SCORE_LAG 1
@@ -40,7 +40,7 @@ constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter o
 #define NACL_SCORE_SPLIT 1
 #endif
 #ifndef NACL_SPLIT_CHUNK
-#define NACL_SPLIT_CHUNK 1024
+#define NACL_SPLIT_CHUNK 2048
 #endif
 constexpr int kSplitChunkKeys = NACL_SPLIT_CHUNK;
 inline bool score_uses_split(int dtype, int D, int P) { return NACL_SCORE_SPLIT && dtype == 1 && D == 128 && P >= 128; }

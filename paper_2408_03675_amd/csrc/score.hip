@@ -741,7 +741,8 @@ __global__ void score_init_kernel(uint32_t* words, int n) {
 // whole tile visible and guarantees that the slot refilled next was read by
 // every wave one step earlier.  An item is kSplitChunkKeys keys; pass 1 needs
 // no merge across waves (each wave owns its proxies' sums over all the
-// item's keys), pass 2 adds the four waves' partial column sums.
+// item's keys), pass 2 adds the four waves' partial column sums every four
+// tiles through a small stage.
 #ifndef NACL_SPLIT_DEPTH
 #define NACL_SPLIT_DEPTH 4
 #endif
@@ -755,9 +756,11 @@ constexpr int kSplitGroup = 16 * kSplitWaveBlocks * kScoreWaves;  // 128 proxies
 static_assert(kSplitTiles % kSplitDepth == 0 && kSplitDepth % 4 == 0, "tiles per item vs ring");
 
 __device__ __forceinline__ void block_barrier() {
-  // A barrier without the fence of __syncthreads(): waits for no memory
-  // operation, so the DMA of later tiles stays in flight across it.
-  asm volatile("s_barrier" ::: "memory");
+  // A barrier without the full fence of __syncthreads(): it waits for this
+  // wave's LDS operations (so LDS writes before it are seen by every wave
+  // after it) but not for its vector memory operations, so the DMA of later
+  // tiles stays in flight across it.
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_kernel(const __bf16* __restrict__ q,
@@ -774,7 +777,8 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kSplitGroup];
   __shared__ float2 mrg[kScoreThreads];
-  __shared__ float col_lds[kScoreWaves][kSplitChunkKeys];
+  __shared__ float col_lds[kSplitChunkKeys];
+  __shared__ float stage[kScoreWaves][64];
   __shared__ __attribute__((aligned(16))) float lse_g[kSplitGroup];
 #define NACL_SSLOT(i) __shared__ __attribute__((aligned(16))) unsigned char sslot##i[KS::kTileBytes];
   NACL_SSLOT(0) NACL_SSLOT(1) NACL_SSLOT(2) NACL_SSLOT(3) NACL_SSLOT(4) NACL_SSLOT(5) NACL_SSLOT(6) NACL_SSLOT(7)
@@ -784,7 +788,6 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const float c2 = a.c2;
-  float* my_cols = col_lds[wave];
   const uint32_t row_bytes = (uint32_t)(a.ks[2] * (int64_t)sizeof(T));
   // This wave's DMA instruction of a tile: rows kRowsPerInstr * wave ...
   uint32_t vo_all[KS::kInstr];
@@ -1091,10 +1094,22 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
           return cs;
         };
         // Partial column sums of the last four tiles; every fourth tile they
-        // are reduced across lane groups and lane group g stores tile t - 3 + g.
+        // are reduced across lane groups (lane group g holds tile t - 3 + g)
+        // and staged per wave; one step later, after the barrier, wave 0 adds
+        // the four waves' stages in a fixed order into the item's columns.
         float cs4[4];
+        auto reduce_stage = [&](int t0) {  // tiles t0 .. t0 + 3
+          if (wave == 0) {
+            const float z = ((stage[0][lane] + stage[1][lane]) + stage[2][lane]) + stage[3][lane];
+            const int idx = t0 * 16 + lane;
+            col_lds[idx] = (g0 == 0 ? 0.f : col_lds[idx]) + z;
+          }
+        };
         k_tiles([&](int t, const frag_t (&kf)[kS], auto u_c) {
           constexpr int u = decltype(u_c)::value;
+          if constexpr (u % 4 == 0) {
+            if (t >= 4) reduce_stage(t - 4);
+          }
           const int key0 = chunk_key0 + 16 * t;
           float cs = 0.f;
           if (key0 <= last) {
@@ -1104,18 +1119,14 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
             else cs = body2(key0, acc, std::false_type{});
           }
           cs4[u % 4] = cs;
-          if constexpr (u % 4 == 3) {
-            const float z = colsum4(cs4[0], cs4[1], cs4[2], cs4[3]);
-            const int idx = (t - 3) * 16 + lane;
-            my_cols[idx] = (g0 == 0 ? 0.f : my_cols[idx]) + z;
-          }
+          if constexpr (u % 4 == 3) stage[wave][lane] = colsum4(cs4[0], cs4[1], cs4[2], cs4[3]);
         });
+        __syncthreads();
+        reduce_stage(kSplitTiles - 4);
       }
       __syncthreads();
       float* F = s.scores + (int64_t)bh * a.L;
-      auto col_of = [&](int idx) -> float {
-        return ((col_lds[0][idx] + col_lds[1][idx]) + col_lds[2][idx]) + col_lds[3][idx];
-      };
+      auto col_of = [&](int idx) -> float { return col_lds[idx]; };
       for (int idx = threadIdx.x; idx < kSplitChunkKeys; idx += kScoreThreads) {
         const int key = chunk_key0 + idx;
         if (key < a.L) F[key] = col_of(idx);
