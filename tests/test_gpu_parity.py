@@ -57,7 +57,7 @@ SCORE_CASES = [
     ("bf16_len1", 1, 1, 1, 64, "bf16", [0]),
     ("bf16_len17", 2, 1, 17, 128, "bf16", [16]),
     # the proxy-split kernel (bf16, D = 128, P >= 128): scattered proxies over several
-    # 1024-key items with a ragged tail, and proxies early so later items lie past them
+    # 2048-key items with a ragged tail, and proxies early so later items lie past them
     ("bf16_split_scattered", 1, 2, 5001, 128, "bf16", sorted(set(range(7, 5001, 31)))),
     ("bf16_split_early", 2, 1, 4100, 128, "bf16", list(range(200, 330))),
 ]
