@@ -273,16 +273,18 @@ def test_evict_is_deterministic():
 
 @pytest.mark.parametrize("mode", [SAMPLE_SOFTMAX, SAMPLE_PROPORTIONAL, SAMPLE_UNIFORM])
 @pytest.mark.parametrize("where", ["end", "early"])
-def test_evict_draws_the_same_keys_as_select(mode, where):
+@pytest.mark.parametrize("P", [40, 160])
+def test_evict_draws_the_same_keys_as_select(mode, where, P):
     """nacl_evict draws the Gumbel keys inside the column reduction (skipping
     the selection's key kernel); its keep set must equal that of nacl_select
     run on the same scores, which draws every key in its own kernel.  Proxies
     at the end, or early so that whole chunks lie past the last proxy (scores
     0, keys drawn on the zero path); L not a multiple of 4; every non-protected
-    slot random, so every key's value matters."""
+    slot random, so every key's value matters.  P = 160 runs the proxy-split
+    score kernel, P = 40 the per-wave-tile one."""
     B, H, L, D = 2, 3, 9001, 128
-    pos = list(range(L - 40, L)) if where == "end" else list(range(300, 340))
-    _say("evict keys", mode, where)
+    pos = list(range(L - P, L)) if where == "end" else list(range(300, 300 + P))
+    _say("evict keys", mode, where, P)
     w = custom("keys", B, H, L, D, len(pos), dtype="bf16", data_seed=61)
     q, k, v = make_layer(w, 0, device="cuda")
     prob = nacl.Problem.from_tensors(q, k, v, pos)
