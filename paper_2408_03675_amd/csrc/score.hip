@@ -749,10 +749,12 @@ __global__ void score_init_kernel(uint32_t* words, int n) {
 #ifndef NACL_SPLIT_OCC
 #define NACL_SPLIT_OCC 4
 #endif
+// Proxy lists at least this long use groups of 512 (eight blocks per wave).
+#ifndef NACL_SPLIT_WIDE_P
+#define NACL_SPLIT_WIDE_P 512
+#endif
 constexpr int kSplitDepth = NACL_SPLIT_DEPTH;                // ring slots per block (at most 8)
 constexpr int kSplitTiles = kSplitChunkKeys / 16;            // tiles per item
-constexpr int kSplitWaveBlocks = 2;                          // proxy blocks of 16 per wave
-constexpr int kSplitGroup = 16 * kSplitWaveBlocks * kScoreWaves;  // 128 proxies
 static_assert(kSplitTiles % kSplitDepth == 0 && kSplitDepth % 4 == 0, "tiles per item vs ring");
 
 __device__ __forceinline__ void block_barrier() {
@@ -763,16 +765,21 @@ __device__ __forceinline__ void block_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-__global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_kernel(const __bf16* __restrict__ q,
-                                                                       const __bf16* __restrict__ k,
-                                                                       ScoreArgs a, ScoreSched s) {
+// WB proxy blocks of 16 per wave, so proxy groups of 64 * WB: WB = 2 (groups
+// of 128, four blocks per CU) or WB = 8 (groups of 512 for long proxy lists,
+// so that K is streamed once per pass instead of once per 128 proxies; two
+// blocks per CU).
+template <int WB>
+__device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, const __bf16* __restrict__ k,
+                                                 const ScoreArgs& a, const ScoreSched& s) {
   using T = __bf16;
   constexpr int D = 128;
   using M = Mma<T, D>;
   using KS = KStage<T, D>;
   using frag_t = typename M::frag_t;
   constexpr int kS = M::kSteps;
-  constexpr int WB = kSplitWaveBlocks;
+  constexpr int kSplitGroup = 16 * WB * kScoreWaves;  // proxies per group
+  constexpr int kNB = WB < 4 ? WB : 4;                // proxy blocks per MFMA batch
   static_assert(KS::kInstr == kScoreWaves, "one DMA instruction per wave and tile");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kSplitGroup];
@@ -908,12 +915,14 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
           ref[pb] = 0.f;
           sm[pb] = 0.f;
         }
-        auto body1 = [&](int t, const f32x4 (&acc)[WB], auto full_c) {
+        // Blocks [P0, P0 + kNB) of one tile (acc[pb - P0]).
+        auto body1 = [&](int t, const f32x4 (&acc)[kNB], auto p0_c, auto full_c) {
+          constexpr int P0 = decltype(p0_c)::value;
           constexpr bool FULL = decltype(full_c)::value;
           const int key0 = chunk_key0 + 16 * t;
           const int* pos_l = pos_g + w0 + opaque(r16);
 #pragma unroll
-          for (int pb = 0; pb < WB; ++pb) {
+          for (int pb = P0; pb < P0 + kNB; ++pb) {
             bool vis[4];
             if constexpr (!FULL) {
               const int pi = pos_l[16 * pb];
@@ -923,13 +932,13 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
             if (t == 0) {
               float mx = -INFINITY;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) mx = (FULL || vis[e]) ? fmaxf(mx, acc[pb][e]) : mx;
+              for (int e = 0; e < 4; ++e) mx = (FULL || vis[e]) ? fmaxf(mx, acc[pb - P0][e]) : mx;
               mx = max_over_groups(mx);
               ref[pb] = mx != -INFINITY ? mx * c2 : 0.f;
             }
             float x[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb][e], c2, -ref[pb]));
+            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb - P0][e], c2, -ref[pb]));
             if constexpr (!FULL) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) x[e] = vis[e] ? x[e] : 0.f;
@@ -940,10 +949,13 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
         k_tiles([&](int t, const frag_t (&kf)[kS], auto) {
           const int key0 = chunk_key0 + 16 * t;
           if (key0 > last) return;
-          f32x4 acc[WB];
-          tile_logits<M, WB, 0, WB, true>(kf, qf, acc);
-          if (key0 + 15 <= first) body1(t, acc, std::true_type{});
-          else body1(t, acc, std::false_type{});
+          static_for<WB / kNB>([&](auto h_c) {
+            using P0 = std::integral_constant<int, decltype(h_c)::value * kNB>;
+            f32x4 acc[kNB];
+            tile_logits<M, WB, P0::value, kNB, true>(kf, qf, acc);
+            if (key0 + 15 <= first) body1(t, acc, P0{}, std::true_type{});
+            else body1(t, acc, P0{}, std::false_type{});
+          });
         });
         bool bad = false;
 #pragma unroll
@@ -965,18 +977,21 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
               if (key0 > last) break;
               frag_t kf[kS];
               M::load_k(rsrc, voff + (uint32_t)key0 * row_bytes, kf);
-              f32x4 acc[WB];
-              tile_logits<M, WB, 0, WB, true>(kf, qf, acc);
+              static_for<WB / kNB>([&](auto h_c) {
+                constexpr int P0 = decltype(h_c)::value * kNB;
+                f32x4 acc[kNB];
+                tile_logits<M, WB, P0, kNB, true>(kf, qf, acc);
 #pragma unroll
-              for (int pb = 0; pb < WB; ++pb) {
-                const int pi = pos_g[w0 + 16 * pb + r16];
+                for (int pb = P0; pb < P0 + kNB; ++pb) {
+                  const int pi = pos_g[w0 + 16 * pb + r16];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                  const bool v = key0 + 4 * g + e <= pi;
-                  if (pass == 0) mx[pb] = v ? fmaxf(mx[pb], acc[pb][e]) : mx[pb];
-                  else sm[pb] += v ? fast_exp2(fmaf(acc[pb][e], c2, -ref[pb])) : 0.f;
+                  for (int e = 0; e < 4; ++e) {
+                    const bool v = key0 + 4 * g + e <= pi;
+                    if (pass == 0) mx[pb] = v ? fmaxf(mx[pb], acc[pb - P0][e]) : mx[pb];
+                    else sm[pb] += v ? fast_exp2(fmaf(acc[pb - P0][e], c2, -ref[pb])) : 0.f;
+                  }
                 }
-              }
+              });
             }
             if (pass == 0) {
 #pragma unroll
@@ -1071,20 +1086,21 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
         __syncthreads();
         // This lane's share of its key's column sum over the wave's proxies;
         // FULL tiles carry no masking.
-        auto body2 = [&](int key0, const f32x4 (&acc)[WB], auto full_c) -> float {
+        auto body2 = [&](int key0, const f32x4 (&acc)[kNB], auto p0_c, auto full_c) -> float {
+          constexpr int P0 = decltype(p0_c)::value;
           constexpr bool FULL = decltype(full_c)::value;
           const int o = w0 + opaque(4 * g);
           const float* lse_l = lse_g + o;
           const int* pos_l = pos_g + o;
-          f32x4 lrs[WB];
+          f32x4 lrs[kNB];
 #pragma unroll
-          for (int pb = 0; pb < WB; ++pb) lrs[pb] = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
+          for (int pb = P0; pb < P0 + kNB; ++pb) lrs[pb - P0] = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
           float cs = 0.f;
 #pragma unroll
-          for (int pb = 0; pb < WB; ++pb) {
+          for (int pb = P0; pb < P0 + kNB; ++pb) {
             float x[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb][e], c2, -lrs[pb][e]));
+            for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[pb - P0][e], c2, -lrs[pb - P0][e]));
             if constexpr (!FULL) {
 #pragma unroll
               for (int e = 0; e < 4; ++e) x[e] = key0 + r16 <= pos_l[16 * pb + e] ? x[e] : 0.f;
@@ -1113,10 +1129,13 @@ __global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_ker
           const int key0 = chunk_key0 + 16 * t;
           float cs = 0.f;
           if (key0 <= last) {
-            f32x4 acc[WB];
-            tile_logits<M, WB, 0, WB, false>(kf, qf, acc);
-            if (key0 + 15 <= first) cs = body2(key0, acc, std::true_type{});
-            else cs = body2(key0, acc, std::false_type{});
+            static_for<WB / kNB>([&](auto h_c) {
+              using P0 = std::integral_constant<int, decltype(h_c)::value * kNB>;
+              f32x4 acc[kNB];
+              tile_logits<M, WB, P0::value, kNB, false>(kf, qf, acc);
+              if (key0 + 15 <= first) cs += body2(key0, acc, P0{}, std::true_type{});
+              else cs += body2(key0, acc, P0{}, std::false_type{});
+            });
           }
           cs4[u % 4] = cs;
           if constexpr (u % 4 == 3) stage[wave][lane] = colsum4(cs4[0], cs4[1], cs4[2], cs4[3]);
@@ -1170,8 +1189,21 @@ int proxy_blocks(int dtype, int D, int P) {
 
 }  // namespace
 
-hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
-  auto kern = score_split_kernel;
+// The two kernels (the launch bound, which sets the register budget, has to
+// be a constant of the kernel itself).
+__global__ __launch_bounds__(kScoreThreads, NACL_SPLIT_OCC) void score_split_kernel(const __bf16* __restrict__ q,
+                                                                                    const __bf16* __restrict__ k,
+                                                                                    ScoreArgs a, ScoreSched s) {
+  score_split_body<2>(q, k, a, s);
+}
+__global__ __launch_bounds__(kScoreThreads, 2) void score_split_wide_kernel(const __bf16* __restrict__ q,
+                                                                           const __bf16* __restrict__ k,
+                                                                           ScoreArgs a, ScoreSched s) {
+  score_split_body<8>(q, k, a, s);
+}
+
+template <class K>
+hipError_t launch_score_split_t(K kern, const ScoreLaunch& L, hipStream_t stream) {
   int per_cu = 0;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kScoreThreads, 0);
   if (e != hipSuccess) return e;
@@ -1186,6 +1218,11 @@ hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
   hipLaunchKernelGGL(kern, dim3(grid), dim3(kScoreThreads), 0, stream, static_cast<const __bf16*>(L.q),
                      static_cast<const __bf16*>(L.k), L.args, L.sched);
   return hipGetLastError();
+}
+
+hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
+  if (L.args.P >= NACL_SPLIT_WIDE_P) return launch_score_split_t(score_split_wide_kernel, L, stream);
+  return launch_score_split_t(score_split_kernel, L, stream);
 }
 
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream) {
