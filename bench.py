@@ -70,7 +70,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(eviction shards by head or batch with no communication; see DESIGN.md)",
+              "(eviction shards by head or batch, with no communication between GPUs)",
               file=sys.stderr)
         sys.exit(2)
 
