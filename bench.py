@@ -63,6 +63,9 @@ def parse():
                     help="run one kernel three times on layer 0 and exit (for rocprofv3 counter runs)")
     ap.add_argument("--pass-breakdown", action="store_true",
                     help="also time the score kernel's second pass alone (caller-supplied LSE)")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the benchmark, print one JSON line per parity workload (GPU times, "
+                         "score roofline fraction, oracle rate on a bounded sample of heads)")
     return ap.parse_args()
 
 
@@ -78,6 +81,9 @@ def main():
     from paper_2408_03675_amd import nacl
     from synth import WORKLOADS, alg_bytes, alg_flops, make_layer
 
+    if args.configs:
+        run_configs()
+        return
     w = WORKLOADS[args.workload]
     layers = args.layers or w.layers
     if args.probe:
@@ -280,6 +286,79 @@ def run_probe(which, w, prob, ws, layer0, out0):
             dst.copy_(src)
     torch.cuda.synchronize()
     log(f"[bench] probe {which} done")
+
+
+def run_configs(oracle_seconds=5.0):
+    """One JSON line per parity workload: nacl_evict and nacl_score times (events, median of
+    repetitions, one layer), the score kernel against its roofline (HBM below the ridge of the
+    input dtype, MFMA above it, executed flops of both passes), and the oracle on the host on as
+    many heads of the same inputs as fit in about oracle_seconds (at least one), scaled to the
+    whole layer."""
+    import statistics
+    import torch
+    from paper_2408_03675_amd import nacl
+    from synth import WORKLOADS, alg_bytes, alg_flops, make_layer, sweep_workloads
+    from oracle import evict as o_evict
+
+    dev = torch.device("cuda:0")
+    nacl.load_library()
+    works = [WORKLOADS["small_f32"], WORKLOADS["longbench_4k"]] + sweep_workloads() + \
+        [WORKLOADS["long_128k"], WORKLOADS["prefill_32k"]]
+    cache = {}
+    for w in works:
+        key = (w.B, w.H, w.L, w.D, w.dtype, w.data_seed, w.inject, w.P)
+        if key not in cache:
+            cache.clear()
+            torch.cuda.empty_cache()
+            cache[key] = make_layer(w, 0, device=dev)
+        q, k, v = cache[key]
+        pos_dev = torch.tensor(w.proxy_pos, dtype=torch.int32, device=dev)
+        prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=w.scale, proxy_pos_dev=pos_dev)
+        ws = nacl.workspace(prob, dev)
+        stream = torch.cuda.current_stream(dev)
+
+        def med_us(fn, reps=7):
+            for _ in range(2):
+                fn()
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            return statistics.median(ts)
+        F = torch.empty((w.B, w.H, w.L), dtype=torch.float32, device=dev)
+        t_ev = med_us(lambda: nacl.evict(prob, q, k, v, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, 0, ws=ws))
+        t_sc = med_us(lambda: nacl.score(prob, q, k, ws, out=F))
+        elt = 4 if w.dtype == "f32" else 2
+        ridge = (F32_PEAK_TFLOPS if w.dtype == "f32" else BF16_PEAK_TFLOPS) * 1e12 / (HBM_PEAK_GBS * 1e9)
+        intensity = 2 * w.P * w.D / (w.D * elt)
+        if intensity < ridge:
+            bound, frac = "hbm", alg_bytes(w)["score"] / (t_sc * 1e3) / HBM_PEAK_GBS
+        else:
+            peak = F32_PEAK_TFLOPS if w.dtype == "f32" else BF16_PEAK_TFLOPS
+            bound, frac = "mfma", 2 * alg_flops(w) / (t_sc * 1e6) / peak
+        # The oracle on heads of batch row 0 (host copies of the same inputs).
+        qh, kh, vh = (t[:1].float().cpu().numpy() for t in (q, k, v))
+        n, spent = 0, 0.0
+        while n < w.H and spent < oracle_seconds:
+            h = n
+            t0 = time.perf_counter()
+            o_evict(qh[:, h:h + 1], kh[:, h:h + 1], vh[:, h:h + 1], w.proxy_pos, w.n_protect, w.C, w.Cr, 0,
+                    w.rng_seed, 0, w.scale)
+            spent += time.perf_counter() - t0
+            n += 1
+        per_head = spent / n
+        line = {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "D": w.D, "P": w.P, "dtype": w.dtype,
+                "C": w.C, "Cr": w.Cr, "evict_us": round(t_ev, 1), "score_us": round(t_sc, 1),
+                "tokens_per_s": round(w.B * w.L / (t_ev * 1e-6), 1),
+                "score_roofline": {"bound": bound, "frac": round(frac, 4)},
+                "oracle_tokens_per_s": round(w.B * w.L / (per_head * w.B * w.H), 1),
+                "oracle_sample": f"{n} of {w.B * w.H} heads, {spent:.1f} s"}
+        print(json.dumps(line), flush=True)
+        del ws, F, qh, kh, vh
 
 
 def cpu_baseline(w, data, seconds):
