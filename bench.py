@@ -149,9 +149,12 @@ def main():
     log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step, {ms_per_step / layers * 1e3:.1f} us/layer")
 
     # Per-stage durations through the public entry points, timed with events
-    # on the launch stream.  nacl_score = score_init_kernel (zeroes the work
-    # queue counters, ~5 us) + the score kernel (score_split_kernel for bf16,
-    # D = 128 and at least 128 proxies, else score_kernel); nacl_select =
+    # on the launch stream.  nacl_score = an init kernel (zeroes the work
+    # queue counters) + the score kernel (score_split_kernel for bf16,
+    # D = 128 and at least 128 proxies, else score_kernel; with
+    # NACL_SCORE_PATH=fused and exactly 128 proxies the opt-in single-read
+    # score_fused_kernel after an init kernel that also zeroes its row-sum
+    # words and computes its references); nacl_select =
     # gumbel_keys_kernel + select_kernel_regs (select_kernel_global past 32k
     # tokens); nacl_compact = compact_kernel.  Inside nacl_evict the score
     # kernel also draws the Gumbel keys and the key kernel is skipped.
@@ -195,6 +198,9 @@ def main():
         raise RuntimeError("score kernel reported a wait that hit its spin limit")
     ab = alg_bytes(w)
     fl = alg_flops(w)
+    fused = w.dtype == "bf16" and w.D == 128 and w.P == 128 and os.environ.get("NACL_SCORE_PATH") == "fused"
+    split = w.dtype == "bf16" and w.D == 128 and w.P >= 128 and not fused
+    passes = 1 if fused else 2  # logit passes the kernel executes
     peak_tf = F32_PEAK_TFLOPS if w.dtype == "f32" else BF16_PEAK_TFLOPS
     stages = {
         "score_us": round(t_score, 2),
@@ -203,7 +209,7 @@ def main():
         "layer_us": round(ms_per_step / layers * 1e3, 2),
         "score_alg_GBps": round(ab["score"] / (t_score * 1e3), 1),
         "score_mfma_frac_alg": round(fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
-        "score_mfma_frac_exec": round(2 * fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
+        "score_mfma_frac_exec": round(passes * fl / (t_score * 1e-6) / (peak_tf * 1e12), 4),
         "select_alg_GBps": round(ab["select"] / (t_select * 1e3), 1),
         "compact_alg_GBps": round(ab["compact"] / (t_compact * 1e3), 1),
         "compact_hbm_frac": round(ab["compact"] / (t_compact * 1e3) / HBM_PEAK_GBS, 4),
@@ -217,8 +223,8 @@ def main():
     # Dominant kernel: the score kernel.  Its roofline is HBM (algorithmic
     # intensity P flop/byte, below the bf16 ridge of ~312): algorithmic bytes
     # = K read once + proxy rows of Q + F written, per launch (one layer).
-    split = w.dtype == "bf16" and w.D == 128 and w.P >= 128
-    dom = {"kernel": "score_split_kernel" if split else "score_kernel", "bound": "hbm", "us": t_score,
+    kname = "score_fused_kernel" if fused else ("score_split_kernel" if split else "score_kernel")
+    dom = {"kernel": kname, "bound": "hbm", "us": t_score,
            "achieved": ab["score"] / (t_score * 1e3), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     traffic = None
     if MEASURED_TRAFFIC and MEASURED_TRAFFIC.get("workload") == w.name and \

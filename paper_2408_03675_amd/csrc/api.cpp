@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -36,7 +37,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
 
 struct Layout {
-  size_t cnt, pos, lse, part, keys, total;
+  size_t cnt, pos, lse, part, keys, fsum, total;
   int n_chunks;
 };
 
@@ -48,7 +49,7 @@ Layout layout_of(const nacl_problem* p) {
   l.n_chunks = (p->L + nacl::kScoreMinChunkKeys - 1) / nacl::kScoreMinChunkKeys;  // most chunks any call uses
   size_t off = 0;
   l.cnt = off;
-  off += align_up((kCounterHeader + BH) * sizeof(uint32_t));
+  off += align_up((kCounterHeader + 2 * BH) * sizeof(uint32_t));  // header, per-head counters, head list
   l.pos = off;
   off += align_up((size_t)p->P * sizeof(int32_t));
   l.lse = off;
@@ -57,6 +58,9 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up(BH * l.n_chunks * p->P * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
+  l.fsum = off;
+  if (nacl::score_fused_shape(p->dtype, p->D, p->P))
+    off += align_up(BH * nacl::kFusedReps * nacl::kFusedProxies * sizeof(uint64_t));
   l.total = off;
   return l;
 }
@@ -194,6 +198,46 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   const int BH = p->B * p->H;
   nacl::ScoreSched& sc = s.sched;
   sc.lse_given = lse != nullptr;
+  uint32_t* words = reinterpret_cast<uint32_t*>(ws + l.cnt);
+  sc.queue = words;
+  sc.status = words + 1;
+  sc.head_cnt = words + kCounterHeader;
+  sc.scores = scores;
+  sc.gkeys = kd.on ? reinterpret_cast<uint32_t*>(ws + l.keys) : nullptr;
+  sc.g_mode = kd.sampling;
+  sc.g_k0 = (uint32_t)(kd.seed & 0xFFFFFFFFu);
+  sc.g_k1 = (uint32_t)(kd.seed >> 32);
+  sc.g_layer = kd.layer;
+  s.n_counter_words = kCounterHeader + BH;
+  // The single-read kernel (bf16, D = 128, 128 proxies, no caller
+  // log-sum-exp, a head's chunks within the resident work-groups) runs when
+  // built in (NACL_SCORE_FUSED) or asked for with NACL_SCORE_PATH=fused;
+  // NACL_SCORE_PATH=split always takes the two-pass kernels, and
+  // NACL_FUSED_PRESUM=1 sums every item ahead of its turn.  The variables
+  // exist for tests and measurements.
+  const char* path_env = std::getenv("NACL_SCORE_PATH");
+  const bool want_fused = path_env ? std::strcmp(path_env, "fused") == 0 : NACL_SCORE_FUSED != 0;
+  if (want_fused && !sc.lse_given && nacl::score_fused_shape(p->dtype, p->D, p->P)) {
+    const int n_chunks = (p->L + nacl::kFusedKeys - 1) / nacl::kFusedKeys;
+    const int n_vis = p->proxy_pos[p->P - 1] / nacl::kFusedKeys + 1;
+    if (n_vis <= nacl::score_fused_resident() && n_vis <= 255 * nacl::kFusedReps) {
+      const char* pre_env = std::getenv("NACL_FUSED_PRESUM");
+      sc.fused = 1;
+      sc.chunk_keys = nacl::kFusedKeys;
+      sc.n_chunks = n_chunks;
+      sc.total_items = BH * n_chunks;
+      sc.n_vis = n_vis;
+      sc.presum = pre_env && std::strcmp(pre_env, "1") == 0;
+      sc.fsums = reinterpret_cast<uint64_t*>(ws + l.fsum);
+      sc.fref = reinterpret_cast<float*>(ws + l.lse);
+      sc.done = words + 2;
+      sc.bad_n = words + 3;
+      sc.bad_list = words + kCounterHeader + BH;
+      hipError_t e = nacl::launch_score(s, stream);
+      if (e != hipSuccess) return hip_fail(e, "score kernel");
+      return NACL_OK;
+    }
+  }
   // Item size: the largest tpw whose items still number at least four per
   // resident work-group (two per CU); long items amortise the per-item Q
   // loads, partial stores and pipeline fill, too few leave a long tail.
@@ -214,21 +258,10 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   sc.n_groups = BH / sc.heads_per_group;
   sc.lag = std::min(NACL_SCORE_LAG, sc.n_groups);
   sc.total_items = passes * BH * sc.n_chunks;
-  uint32_t* words = reinterpret_cast<uint32_t*>(ws + l.cnt);
-  sc.queue = words;
-  sc.status = words + 1;
-  sc.head_cnt = words + kCounterHeader;
   sc.partials = reinterpret_cast<float2*>(ws + l.part);
   sc.lse2 = reinterpret_cast<float*>(ws + l.lse);
   sc.lse_in = lse;
   sc.lse_mul = 1.4426950408889634f;
-  sc.scores = scores;
-  sc.gkeys = kd.on ? reinterpret_cast<uint32_t*>(ws + l.keys) : nullptr;
-  sc.g_mode = kd.sampling;
-  sc.g_k0 = (uint32_t)(kd.seed & 0xFFFFFFFFu);
-  sc.g_k1 = (uint32_t)(kd.seed >> 32);
-  sc.g_layer = kd.layer;
-  s.n_counter_words = kCounterHeader + BH;
   hipError_t e = nacl::launch_score(s, stream);
   if (e != hipSuccess) return hip_fail(e, "score kernel");
   return NACL_OK;
