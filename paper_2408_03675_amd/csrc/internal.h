@@ -29,7 +29,7 @@ namespace nacl {
 #endif
 // Tiles per wave and item: chosen per call among kScoreTpwMin * 2^i up to
 // kScoreTpwMax.  The workspace is sized for the smallest.
-constexpr int kScoreTpwMin = 32;
+constexpr int kScoreTpwMin = 8;
 constexpr int kScoreTpwMax = NACL_SCORE_TPW_MAX;
 constexpr int kScoreWavesPerSimd = NACL_SCORE_WAVES;
 constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter of the item's keys
