@@ -1084,6 +1084,15 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
         for (int i = threadIdx.x; i < kSplitGroup; i += kScoreThreads)
           lse_g[i] = i < gn ? load_coherent(lse + (int64_t)bh * a.P + g0 + i) * lse_mul : INFINITY;
         __syncthreads();
+        // With groups of 128 proxies this lane's eight log-sum-exps (rows
+        // 4 g + e of its two proxy blocks) stay in registers for the whole
+        // item; wider groups read them from LDS at every tile.
+        constexpr int kLR = WB == 2 ? WB : 1;
+        f32x4 lse_r[kLR];
+        if constexpr (WB == 2) {
+#pragma unroll
+          for (int pb = 0; pb < kLR; ++pb) lse_r[pb] = *reinterpret_cast<const f32x4*>(lse_g + w0 + 4 * g + 16 * pb);
+        }
         // This lane's share of its key's column sum over the wave's proxies;
         // FULL tiles carry no masking.
         auto body2 = [&](int key0, const f32x4 (&acc)[kNB], auto p0_c, auto full_c) -> float {
@@ -1093,8 +1102,13 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
           const float* lse_l = lse_g + o;
           const int* pos_l = pos_g + o;
           f32x4 lrs[kNB];
+          if constexpr (WB == 2) {
 #pragma unroll
-          for (int pb = P0; pb < P0 + kNB; ++pb) lrs[pb - P0] = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
+            for (int pb = P0; pb < P0 + kNB; ++pb) lrs[pb - P0] = lse_r[pb < kLR ? pb : 0];
+          } else {
+#pragma unroll
+            for (int pb = P0; pb < P0 + kNB; ++pb) lrs[pb - P0] = *reinterpret_cast<const f32x4*>(lse_l + 16 * pb);
+          }
           float cs = 0.f;
 #pragma unroll
           for (int pb = P0; pb < P0 + kNB; ++pb) {
