@@ -100,8 +100,14 @@ size_t nacl_workspace_bytes(const nacl_problem* p);
  * Health word: once the stream has completed the call, the 32-bit word at
  * byte offset 4 of the workspace is 0.  Bit 0 set means a wave of the
  * two-pass kernel gave up waiting for a head's log-sum-exp after its bounded
- * spin (never expected; the scores of that call are then not valid).  The
- * next nacl_score or nacl_evict call on the workspace clears it. */
+ * spin, bit 1 the same for the single-read kernel's wait for a head's row
+ * sums (never expected; the scores of that call are then not valid).  The
+ * next nacl_score or nacl_evict call on the workspace clears it.
+ * Kernel choice (also inside nacl_evict): two passes over K by default.  For
+ * bf16, D = 128, exactly 128 proxies and lse == NULL, the environment
+ * variable NACL_SCORE_PATH=fused selects a kernel that reads K once (same
+ * results within the tolerance, slower on MI355X); NACL_SCORE_PATH=split
+ * forces the two-pass kernels.  Both are meant for tests and measurements. */
 int nacl_score(const nacl_problem* p, const void* q, const void* k, const float* lse,
                float* scores, void* ws, size_t ws_bytes, void* stream);
 
