@@ -295,8 +295,8 @@ def run_probe(which, w, prob, ws, layer0, out0):
 
 
 def run_configs(oracle_seconds=5.0):
-    """One JSON line per parity workload: nacl_evict and nacl_score times (events, median of
-    repetitions, one layer), the score kernel against its roofline (HBM below the ridge of the
+    """One JSON line per parity workload: nacl_evict and nacl_score times (events around ten
+    back-to-back calls on one layer, median of three such rounds), the score kernel against its roofline (HBM below the ridge of the
     input dtype, MFMA above it, executed flops of both passes), and the oracle on the host on as
     many heads of the same inputs as fit in about oracle_seconds (at least one), scaled to the
     whole layer."""
@@ -323,17 +323,21 @@ def run_configs(oracle_seconds=5.0):
         ws = nacl.workspace(prob, dev)
         stream = torch.cuda.current_stream(dev)
 
-        def med_us(fn, reps=7):
-            for _ in range(2):
+        def med_us(fn, reps=10, rounds=3):
+            # Back-to-back calls between two events (as the benchmark's stage
+            # timing), median over rounds of the per-call average.
+            for _ in range(3):
                 fn()
             ts = []
-            for _ in range(reps):
+            for _ in range(rounds):
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
                 e0.record(stream)
-                fn()
+                for _ in range(reps):
+                    fn()
                 e1.record(stream)
                 torch.cuda.synchronize()
-                ts.append(e0.elapsed_time(e1) * 1e3)
+                ts.append(e0.elapsed_time(e1) * 1e3 / reps)
             return statistics.median(ts)
         F = torch.empty((w.B, w.H, w.L), dtype=torch.float32, device=dev)
         t_ev = med_us(lambda: nacl.evict(prob, q, k, v, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, 0, ws=ws))
