@@ -1193,8 +1193,8 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
 // n runs after the first pass of item n + 1 and normally finds its head
 // complete.  K tiles of the next item are loaded into LDS (one of two 32 KB
 // buffers) while the current item waits and reduces.  Wave 0 issues no K
-// loads; it takes tickets, reads the sum words and adds the row sums, so its
-// memory waits never wait on K.
+// loads; it takes tickets, reads the sum words and writes F, so its memory
+// waits never wait on K.  Wave 1 adds the row sums (fire and forget).
 //
 // Progress: before a work-group waits for head h it holds two items whose
 // sums are in (or in earlier heads), and any item it has taken but not yet
