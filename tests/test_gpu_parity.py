@@ -9,6 +9,7 @@ compacted rows bit-exact.
 
 import sys
 import zlib
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -67,6 +68,11 @@ SCORE_CASES = [
     ("bf16_fused_scattered", 1, 2, 5001, 128, "bf16", [7 + 39 * i for i in range(128)]),
     ("bf16_fused_early", 2, 1, 4100, 128, "bf16", list(range(200, 328))),
     ("bf16_fused_first", 1, 3, 300, 128, "bf16", list(range(128))),
+    # more than 512 proxies: the wide proxy-split kernel over two and three groups of 512
+    # (column sums accumulated across groups), and the per-wave-tile kernel for fp32
+    ("bf16_wide_two_groups", 1, 2, 3000, 128, "bf16", sorted(set(range(5, 3000, 5)))),
+    ("bf16_wide_three_groups", 1, 1, 2300, 128, "bf16", list(range(1200, 2300))),
+    ("f32_many_proxies", 1, 2, 1500, 64, "f32", list(range(800, 1500))),
 ]
 
 
@@ -304,6 +310,15 @@ def test_evict_small_f32_all_heads():
 
 def test_evict_longbench_all_heads():
     _evict_and_compare(WORKLOADS["longbench_4k"], label="longbench_4k")
+
+
+def test_evict_many_protected_proxies():
+    """599 proxies, all protected (the wide score kernel over two groups of 512; the
+    selection excludes 599 tokens from both draws): scores, keep sets and compacted rows
+    against the oracle on every head."""
+    w = custom("evict_many_proxies", 1, 2, 3000, 128, 599, keep_frac=Fraction(1, 2),
+               random_share=Fraction(1, 5), inject=True, data_seed=17)
+    _evict_and_compare(w, label="many proxies")
 
 
 def test_evict_is_deterministic():
