@@ -73,6 +73,7 @@ SCORE_CASES = [
     ("bf16_wide_two_groups", 1, 2, 3000, 128, "bf16", sorted(set(range(5, 3000, 5)))),
     ("bf16_wide_three_groups", 1, 1, 2300, 128, "bf16", list(range(1200, 2300))),
     ("f32_many_proxies", 1, 2, 1500, 64, "f32", list(range(800, 1500))),
+    ("bf16_d64_three_groups", 1, 2, 1200, 64, "bf16", list(range(900, 1200))),
 ]
 
 
