@@ -143,3 +143,24 @@ def test_long_128k():
     _properties(w, F, keep)
     n = _check_heads(w, 0, q, k, v, F, keep, ko, vo, [(0, 0), (0, 29)], "128k")
     _say(f"  128k: {n} near-tie differences")
+
+
+def test_size_limits():
+    """The API's limits: P = 4096 proxies (every token of a 4096-token head, the H2O-like
+    case; the wide kernel over eight groups of 512), and one head of L = 2^19 tokens
+    through the whole eviction (the selection kernel that re-reads keys from memory)."""
+    from synth import custom
+    w = custom("p_limit", 1, 1, 4096, 128, 4096, dtype="bf16", data_seed=21)
+    q, k, v = make_layer(w, 0, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=w.scale)
+    F = nacl.score(prob, q, k, nacl.workspace(prob))
+    torch.cuda.synchronize()
+    Fr, _ = proxy_scores(_f64(q), _f64(k), w.proxy_pos, w.scale)
+    check_scores(F.cpu().numpy(), Fr, "P = 4096")
+
+    w = custom("l_limit", 1, 1, 1 << 19, 128, 16, dtype="bf16", inject=True, data_seed=22)
+    _say("L = 2^19 eviction")
+    q, k, v, F, keep, ko, vo = _evict(w, 0)
+    _properties(w, F, keep)
+    n = _check_heads(w, 0, q, k, v, F, keep, ko, vo, [(0, 0)], "L = 2^19")
+    _say(f"  1 head compared, {n} near-tie differences")
