@@ -214,6 +214,7 @@ SELECT_CASES = [
     ("ties_heavy", 5000, 8, 8, 1000, 300, SAMPLE_SOFTMAX, True),
     ("ties_uniform", 2500, 8, 4, 700, 100, SAMPLE_UNIFORM, True),
     ("tiny", 5, 1, 1, 3, 1, SAMPLE_SOFTMAX, False),
+    ("empty_budget", 100, 4, 0, 0, 0, SAMPLE_SOFTMAX, False),
     # long heads (keys held in registers up to 32k tokens), ties, extreme budgets
     ("long_softmax", 20000, 128, 128, 4000, 2000, SAMPLE_SOFTMAX, False),
     ("long_proportional", 9001, 40, 20, 1800, 600, SAMPLE_PROPORTIONAL, False),
@@ -313,6 +314,19 @@ def test_evict_small_f32_all_heads():
 
 def test_evict_longbench_all_heads():
     _evict_and_compare(WORKLOADS["longbench_4k"], label="longbench_4k")
+
+
+def test_evict_empty_budget():
+    """C = 0 (nothing kept, no proxy protected): the scores are still computed, the keep
+    set and the compacted cache are empty."""
+    w = custom("empty", 1, 2, 600, 128, 8, dtype="bf16", data_seed=4)
+    q, k, v = make_layer(w, 0, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, n_protect=0)
+    F, keep, ko, vo = nacl.evict(prob, q, k, v, 0, 0, SAMPLE_SOFTMAX, 0, 0, ws=nacl.workspace(prob))
+    torch.cuda.synchronize()
+    assert tuple(keep.shape) == (1, 2, 0) and tuple(ko.shape) == (1, 2, 0, 128) and ko.numel() == 0
+    Fr, _ = proxy_scores(_np(q), _np(k), w.proxy_pos, prob.c.sm_scale)
+    check_scores(F.cpu().numpy(), Fr, "empty budget")
 
 
 def test_evict_many_protected_proxies():
