@@ -97,6 +97,25 @@ def _stream(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
+def _gpu(t, name, dev, shape=None, dtype=None, strides=None, contiguous=False):
+    """Checks a tensor argument before its address reaches the kernels: on the
+    call's GPU, of the expected shape and dtype, with the problem's strides (Q,
+    K, V) or contiguous (scores, indices, outputs, workspace)."""
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a tensor on the GPU")
+    if t.device != dev:
+        raise ValueError(f"{name} is on {t.device}, the call runs on {dev}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if strides is not None and (t.dim() != 4 or t.stride(3) != 1 or tuple(t.stride()[:3]) != tuple(strides)):
+        raise ValueError(f"{name} has strides {tuple(t.stride())}, the problem has {tuple(strides)} (+ 1)")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
 def _strides(t):
     if t.dim() != 4 or t.stride(3) != 1:
         raise ValueError("Q/K/V must be [B, H, L, D] with a contiguous last dimension")
@@ -123,6 +142,11 @@ class Problem:
         s.k_stride[:] = k_stride or dense
         s.v_stride[:] = v_stride or dense
         s.proxy_pos = ctypes.cast(self._pos, ctypes.POINTER(ctypes.c_int32))
+        if proxy_pos_dev is not None:
+            if not (isinstance(proxy_pos_dev, torch.Tensor) and proxy_pos_dev.is_cuda and
+                    proxy_pos_dev.dtype == torch.int32 and proxy_pos_dev.is_contiguous() and
+                    proxy_pos_dev.numel() == len(pos)):
+                raise ValueError("proxy_pos_dev must be a contiguous int32 GPU tensor with one entry per proxy")
         self._pos_dev = proxy_pos_dev
         s.proxy_pos_dev = None if proxy_pos_dev is None else proxy_pos_dev.data_ptr()
         self.c = s
@@ -156,6 +180,11 @@ class Problem:
     def ref(self):
         return ctypes.byref(self.c)
 
+    # Shapes the entry points expect.
+    def qkv(self, t, name, dev, which):
+        st = {"q": self.c.q_stride, "k": self.c.k_stride, "v": self.c.v_stride}[which]
+        return _gpu(t, name, dev, (self.B, self.H, self.L, self.D), self.torch_dtype, tuple(st))
+
 
 def workspace_bytes(prob):
     return int(load_library().nacl_workspace_bytes(prob.ref()))
@@ -173,8 +202,15 @@ def score(prob, q, k, ws, lse=None, out=None):
     """F [B, H, L] fp32 (Section 5.1).  lse: optional [B, H, P] natural
     log-sum-exp from the caller."""
     lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    prob.qkv(q, "q", dev, "q")
+    prob.qkv(k, "k", dev, "k")
+    if lse is not None:
+        _gpu(lse, "lse", dev, (prob.B, prob.H, prob.c.P), torch.float32, contiguous=True)
+    _gpu(ws, "ws", dev, dtype=torch.uint8, contiguous=True)
     if out is None:
         out = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=k.device)
+    _gpu(out, "out", dev, (prob.B, prob.H, prob.L), torch.float32, contiguous=True)
     _check(lib.nacl_score(prob.ref(), _ptr(q), _ptr(k), _ptr(lse), _ptr(out), _ptr(ws),
                           ws.numel(), _stream(k.device)))
     return out
@@ -183,8 +219,12 @@ def score(prob, q, k, ws, lse=None, out=None):
 def select(prob, scores, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=None, out=None):
     """keep_idx [B, H, C] int32, ascending (Sections 5.1-5.2, Algorithm 1)."""
     lib = load_library()
+    dev = _gpu(scores, "scores", scores.device, (prob.B, prob.H, prob.L), torch.float32, contiguous=True).device
+    if ws is not None:
+        _gpu(ws, "ws", dev, dtype=torch.uint8, contiguous=True)
     if out is None:
         out = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=scores.device)
+    _gpu(out, "out", dev, (prob.B, prob.H, int(C)), torch.int32, contiguous=True)
     _check(lib.nacl_select(prob.ref(), _ptr(scores), int(C), int(Cr), int(sampling), int(seed),
                            int(layer), _ptr(out), _ptr(ws), 0 if ws is None else ws.numel(),
                            _stream(scores.device)))
@@ -194,11 +234,17 @@ def select(prob, scores, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
 def compact(prob, k, v, keep_idx, k_out=None, v_out=None):
     """K', V' [B, H, C, D] (Section 3)."""
     lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    prob.qkv(k, "k", dev, "k")
+    prob.qkv(v, "v", dev, "v")
     C = keep_idx.shape[-1]
+    _gpu(keep_idx, "keep_idx", dev, (prob.B, prob.H, C), torch.int32, contiguous=True)
     if k_out is None:
         k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=k.device)
     if v_out is None:
         v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=v.device)
+    for t, name in ((k_out, "k_out"), (v_out, "v_out")):
+        _gpu(t, name, dev, (prob.B, prob.H, C, prob.D), prob.torch_dtype, contiguous=True)
     _check(lib.nacl_compact(prob.ref(), _ptr(k), _ptr(v), _ptr(keep_idx), int(C), _ptr(k_out),
                             _ptr(v_out), _stream(k.device)))
     return k_out, v_out
@@ -209,7 +255,9 @@ def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
     """score -> select -> compact on the current stream.  Returns
     (scores, keep_idx, k_out, v_out)."""
     lib = load_library()
-    dev = k.device
+    dev = _gpu(k, "k", k.device).device
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        prob.qkv(t, name, dev, name)
     if ws is None:
         ws = workspace(prob, dev)
     if scores is None:
@@ -220,6 +268,11 @@ def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
         k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=dev)
     if v_out is None:
         v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=dev)
+    _gpu(ws, "ws", dev, dtype=torch.uint8, contiguous=True)
+    _gpu(scores, "scores", dev, (prob.B, prob.H, prob.L), torch.float32, contiguous=True)
+    _gpu(keep_idx, "keep_idx", dev, (prob.B, prob.H, int(C)), torch.int32, contiguous=True)
+    for t, name in ((k_out, "k_out"), (v_out, "v_out")):
+        _gpu(t, name, dev, (prob.B, prob.H, int(C), prob.D), prob.torch_dtype, contiguous=True)
     _check(lib.nacl_evict(prob.ref(), _ptr(q), _ptr(k), _ptr(v), int(C), int(Cr), int(sampling),
                           int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(k_out),
                           _ptr(v_out), _ptr(ws), ws.numel(), _stream(dev)))

@@ -376,3 +376,23 @@ def test_evict_draws_the_same_keys_as_select(mode, where, P, monkeypatch):
         keep2 = nacl.select(prob, F, C, Cr, mode, 11, 2, ws=nacl.workspace(prob))
         torch.cuda.synchronize()
         assert torch.equal(keep, keep2), (mode, where, Cr)
+
+
+def test_binding_refuses_mismatched_tensors():
+    """Wrong output shapes, dtypes or input strides raise before any launch."""
+    w = custom("binding", 1, 2, 300, 128, 8, dtype="bf16", data_seed=6)
+    q, k, v = make_layer(w, 0, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos)
+    ws = nacl.workspace(prob)
+    with pytest.raises(ValueError, match="shape"):
+        nacl.score(prob, q, k, ws, out=torch.empty((1, 2, 299), device="cuda"))
+    with pytest.raises(ValueError, match="dtype"):
+        nacl.select(prob, torch.zeros((1, 2, 300), device="cuda", dtype=torch.float64), 60, 10, ws=ws)
+    with pytest.raises(ValueError, match="strides"):
+        nacl.score(prob, q, k.transpose(1, 2).contiguous().transpose(1, 2), ws)
+    with pytest.raises(ValueError, match="shape"):
+        nacl.evict(prob, q, k, v, 60, 10, ws=ws, k_out=torch.empty((1, 2, 59, 128), device="cuda",
+                                                                  dtype=torch.bfloat16))
+    F = nacl.score(prob, q, k, ws)  # the same call with matching tensors runs
+    torch.cuda.synchronize()
+    assert torch.isfinite(F).all()
