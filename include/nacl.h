@@ -51,7 +51,7 @@ extern "C" {
 typedef enum {
   NACL_OK = 0,
   NACL_ERR_INVALID_ARG = 1,  /* an argument is out of range or inconsistent */
-  NACL_ERR_UNSUPPORTED = 2,  /* valid in principle, not supported by this build */
+  NACL_ERR_UNSUPPORTED = 2,  /* valid in principle, not supported by the library */
   NACL_ERR_WORKSPACE = 3,    /* workspace missing, misaligned or too small */
   NACL_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
 } nacl_status;
