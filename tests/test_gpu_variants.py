@@ -58,7 +58,7 @@ def _compare_eviction(q_full, k, v, pos, n_protect, C, Cr, mode, seed, layer, sc
         for h in range(H):
             Fr32 = Fr[b, h].astype(np.float32)
             ref = select_head(Fr32, pos, n_protect, C, Cr, mode, seed, layer, b, h)
-            n_diff += check_keep_near(kg[b, h], ref, Fr32, Cr, f"{label} keep b={b} h={h}")
+            n_diff += check_keep_near(kg[b, h], ref, Fr32, Cr, f"{label} keep b={b} h={h}", mode=mode)
             kbits = k[b, h].cpu().view(view).numpy()
             vbits = v[b, h].cpu().view(view).numpy()
             check_rows_for_common(kg[b, h], ko[b, h].cpu().view(view).numpy(), ref["keep"],

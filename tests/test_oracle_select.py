@@ -12,7 +12,8 @@ import pytest
 import scipy.stats
 
 from oracle import (SAMPLE_PROPORTIONAL, SAMPLE_SOFTMAX, SAMPLE_UNIFORM,
-                    budget_split, compact, select, select_head, top_k_lower_index)
+                    budget_split, compact, protected_set, select, select_head,
+                    top_k_lower_index)
 from oracle.sampling import sequential_sample, set_probabilities
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "paper_numbers.json")
@@ -208,3 +209,36 @@ def test_compact_is_exact_row_copy():
                 assert Kc[b, h, c].tobytes() == K[b, h, idx[b, h, c]].tobytes()
                 assert Vc[b, h, c].tobytes() == V[b, h, idx[b, h, c]].tobytes()
     assert Kc.nbytes == B * H * C * D * 4
+
+
+def test_protected_set_is_the_last_proxies():
+    """Reading of "Protect Proxy" (Appendix A.6) with Section 5.1's default
+    (proxies are kept): the force-kept set is the last n_protect proxies in
+    position order, none for n_protect = 0, all of them for n_protect = P.
+    Expected sets are written out, not computed by slicing."""
+    pos = [3, 8, 20, 41, 77]
+    expected = {0: [], 1: [77], 2: [41, 77], 4: [8, 20, 41, 77], 5: [3, 8, 20, 41, 77]}
+    for n, want in expected.items():
+        assert protected_set(pos, n).tolist() == want, n
+    for bad in (-1, 6):
+        with pytest.raises(ValueError):
+            protected_set(pos, bad)
+
+
+def test_unprotected_proxy_competes_in_R():
+    """With n_protect < P the first P - n_protect proxies are ordinary
+    candidates of R (Section 5.1 argmax over R): an unprotected proxy with the
+    largest score is taken by u_score, one with a tiny score is not kept, and
+    a protected proxy with score 0 is kept anyway."""
+    L, C, Cr = 40, 8, 0
+    pos = [30, 31, 32, 33]                # proxies; the last two are protected
+    F = np.full(L, 0.01, dtype=np.float32)
+    F[30] = 5.0                           # unprotected proxy, top score
+    F[31] = 1e-6                          # unprotected proxy, bottom score
+    F[32] = 0.0                           # protected proxy, score 0
+    F[[2, 9, 17, 25, 38]] = [0.5, 0.4, 0.3, 0.2, 0.1]
+    r = select_head(F, pos, 2, C, Cr, SAMPLE_SOFTMAX, 0, 0, 0, 0)
+    assert r["protected"].tolist() == [32, 33]
+    assert r["u_score"].tolist() == [2, 9, 17, 25, 30, 38]
+    assert r["keep"].tolist() == [2, 9, 17, 25, 30, 32, 33, 38]
+    assert 31 not in r["keep"]
