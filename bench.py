@@ -79,6 +79,7 @@ def main():
 
     import torch
     from paper_2408_03675_amd import nacl
+    from paper_2408_03675_amd.layer_loop import LayerLoop
     from synth import WORKLOADS, alg_bytes, alg_flops, make_layer
 
     if args.configs:
@@ -101,35 +102,17 @@ def main():
     q0, k0, v0 = data[0]
     pos_dev = torch.tensor(w.proxy_pos, dtype=torch.int32, device=dev)
     prob = nacl.Problem.from_tensors(q0, k0, v0, w.proxy_pos, sm_scale=w.scale, proxy_pos_dev=pos_dev)
-    ws = nacl.workspace(prob, dev)
-    n_streams = max(1, args.streams)
-    side = [torch.cuda.Stream(dev) for _ in range(n_streams)]  # default priority
-    wss = [ws] + [nacl.workspace(prob, dev) for _ in range(n_streams - 1)]
-    BH = w.B * w.H
-    outs = []
-    for _ in range(layers):
-        outs.append((torch.empty((w.B, w.H, w.L), dtype=torch.float32, device=dev),
-                     torch.empty((w.B, w.H, w.C), dtype=torch.int32, device=dev),
-                     torch.empty((w.B, w.H, w.C, w.D), dtype=q0.dtype, device=dev),
-                     torch.empty((w.B, w.H, w.C, w.D), dtype=q0.dtype, device=dev)))
+    loop = LayerLoop(prob, data, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, streams=args.streams, device=dev)
+    n_streams = len(loop.streams)
+    ws = loop.workspaces[0]
+    outs = loop.outs
 
     if args.probe:
         run_probe(args.probe, w, prob, ws, data[0], outs[0])
         return
 
     stream = torch.cuda.current_stream(dev)
-
-    def step():
-        for s in side:
-            s.wait_stream(stream)
-        for l in range(layers):
-            with torch.cuda.stream(side[l % n_streams]):
-                q, k, v = data[l]
-                F, keep, ko, vo = outs[l]
-                nacl.evict(prob, q, k, v, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, l, ws=wss[l % n_streams],
-                           scores=F, keep_idx=keep, k_out=ko, v_out=vo)
-        for s in side:
-            stream.wait_stream(s)
+    step = loop.run
 
     for i in range(args.warmup):
         step()
@@ -151,10 +134,7 @@ def main():
     # Per-stage durations through the public entry points, timed with events
     # on the launch stream.  nacl_score = an init kernel (zeroes the work
     # queue counters) + the score kernel (score_split_kernel for bf16,
-    # D = 128 and at least 128 proxies, else score_kernel; with
-    # NACL_SCORE_PATH=fused and exactly 128 proxies the opt-in single-read
-    # score_fused_kernel after an init kernel that also zeroes its row-sum
-    # words and computes its references); nacl_select =
+    # D = 128 and at least 128 proxies, else score_kernel); nacl_select =
     # gumbel_keys_kernel + select_kernel_regs (select_kernel_global past 32k
     # tokens); nacl_compact = compact_kernel.  Inside nacl_evict the score
     # kernel also draws the Gumbel keys and the key kernel is skipped.
@@ -193,14 +173,15 @@ def main():
         t_pass2 = timed(f_pass2)
     step()  # restore the real outputs of every layer
     torch.cuda.synchronize()
-    status = max(int(x[4:8].view(torch.int32).item()) for x in wss)
+    # Sticky health words: every call since the workspaces were zeroed,
+    # warm-up and timed steps included, completed its waits normally.
+    status = loop.health()
     if status:
-        raise RuntimeError("score kernel reported a wait that hit its spin limit")
+        raise RuntimeError(f"a kernel reported health bits {status:#x}; the timed results are invalid")
     ab = alg_bytes(w)
     fl = alg_flops(w)
-    fused = w.dtype == "bf16" and w.D == 128 and w.P == 128 and os.environ.get("NACL_SCORE_PATH") == "fused"
-    split = w.dtype == "bf16" and w.D == 128 and w.P >= 128 and not fused
-    passes = 1 if fused else 2  # logit passes the kernel executes
+    split = w.dtype == "bf16" and w.D == 128 and w.P >= 128
+    passes = 2  # logit passes the kernel executes
     peak_tf = F32_PEAK_TFLOPS if w.dtype == "f32" else BF16_PEAK_TFLOPS
     stages = {
         "score_us": round(t_score, 2),
@@ -223,7 +204,7 @@ def main():
     # Dominant kernel: the score kernel.  Its roofline is HBM (algorithmic
     # intensity P flop/byte, below the bf16 ridge of ~312): algorithmic bytes
     # = K read once + proxy rows of Q + F written, per launch (one layer).
-    kname = "score_fused_kernel" if fused else ("score_split_kernel" if split else "score_kernel")
+    kname = ("score_split_wide_kernel" if w.P >= 512 else "score_split_kernel") if split else "score_kernel"
     dom = {"kernel": kname, "bound": "hbm", "us": t_score,
            "achieved": ab["score"] / (t_score * 1e3), "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     traffic = None
@@ -371,14 +352,27 @@ def run_configs(oracle_seconds=5.0):
         del ws, F, qh, kh, vh
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(w, data, seconds):
     """The oracle, as it stands, on whole layers of the same workload (host
     copies of the GPU inputs), layer after layer until `seconds` have passed
     (at least one layer).  tokens/s = B * L * layers done / time, the same
-    per-layer rate as the GPU figure."""
-    import numpy as np
-    from threadpoolctl import threadpool_info
+    per-layer rate as the GPU figure.  Also a one-thread run of the 4k
+    LongBench-shaped layer (a per-core figure)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
     from oracle import evict as o_evict
+    from synth import WORKLOADS, make_layer
 
     done, spent = 0, 0.0
     for l, (q, k, v) in enumerate(data):
@@ -392,11 +386,21 @@ def cpu_baseline(w, data, seconds):
             break
     blas = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
     threads = max(blas) if blas else 1
+    # One thread on the 4k LongBench-shaped layer: the per-core figure.
+    w2 = WORKLOADS["longbench_4k"]
+    q2, k2, v2 = (t.float().numpy() for t in make_layer(w2, 0, device="cpu"))
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        o_evict(q2, k2, v2, w2.proxy_pos, w2.n_protect, w2.C, w2.Cr, 0, w2.rng_seed, 0, w2.scale)
+        t1 = time.perf_counter() - t0
     return {"value": round(w.B * w.L * done / spent, 1), "unit": "tokens/s", "cores": int(threads),
             "kind": "oracle",
             "sample": f"{done} whole layer(s) of {w.name} (all {w.B * w.H} heads each), float64 NumPy "
                       f"oracle, {spent:.1f} s; BLAS on {threads} threads, elementwise work single-threaded",
-            "host_cpus": len(os.sched_getaffinity(0))}
+            "cpu_model": _cpu_model(),
+            "host_cpus": len(os.sched_getaffinity(0)),
+            "one_thread": {"workload": w2.name, "value": round(w2.B * w2.L / t1, 1), "unit": "tokens/s",
+                           "cores": 1, "seconds": round(t1, 2)}}
 
 
 if __name__ == "__main__":

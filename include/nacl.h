@@ -30,7 +30,8 @@
  *   16-byte aligned.
  * - Scores are fp32 [B, H, L] contiguous; keep_idx is int32 [B, H, C]
  *   contiguous, strictly ascending per head; k_out / v_out are [B, H, C, D]
- *   contiguous in the input dtype and must not overlap any input.
+ *   contiguous in the input dtype and overlap no input, or are K and V
+ *   themselves (in-place compaction, see nacl_compact).
  * - Overlapping calls that share a workspace race; give concurrent calls
  *   their own workspaces.
  */
@@ -44,7 +45,7 @@
 extern "C" {
 #endif
 
-#define NACL_VERSION 1
+#define NACL_VERSION 2
 #define NACL_MAX_P 4096          /* proxy tokens per head */
 #define NACL_MAX_L (1 << 19)     /* prompt length */
 
@@ -97,17 +98,15 @@ size_t nacl_workspace_bytes(const nacl_problem* p);
  * it only the column reduction runs.  NULL: the library computes it (two
  * passes over K).  scores: device fp32 [B,H,L], fully overwritten; keys after
  * the last proxy get 0.
- * Health word: once the stream has completed the call, the 32-bit word at
- * byte offset 4 of the workspace is 0.  Bit 0 set means a wave of the
- * two-pass kernel gave up waiting for a head's log-sum-exp after its bounded
- * spin, bit 1 the same for the single-read kernel's wait for a head's row
- * sums (never expected; the scores of that call are then not valid).  The
- * next nacl_score or nacl_evict call on the workspace clears it.
- * Kernel choice (also inside nacl_evict): two passes over K by default.  For
- * bf16, D = 128, exactly 128 proxies and lse == NULL, the environment
- * variable NACL_SCORE_PATH=fused selects a kernel that reads K once (same
- * results within the tolerance, slower on MI355X); NACL_SCORE_PATH=split
- * forces the two-pass kernels.  Both are meant for tests and measurements. */
+ * Health words (score and evict calls): uint32 word 1 of the workspace
+ * (byte offset 4) is this call's, cleared by the call itself; word 2 (byte
+ * offset 8) is sticky: every call ORs its bits into it and no call clears it,
+ * so it covers every call since the caller last zeroed it (zero it when the
+ * workspace is allocated; the Python binding does).  Bit 0: a wave gave up
+ * waiting for a head's log-sum-exp after its bounded spin.  Bit 2 (evict
+ * only): the compaction met a keep index outside [0, L).  Never expected;
+ * whenever a call's word is non-zero once the stream has completed it, that
+ * call's scores, keep_idx, k_out and v_out are not valid. */
 int nacl_score(const nacl_problem* p, const void* q, const void* k, const float* lse,
                float* scores, void* ws, size_t ws_bytes, void* stream);
 
@@ -126,23 +125,42 @@ int nacl_select(const nacl_problem* p, const float* scores, int32_t C, int32_t C
                 void* ws, size_t ws_bytes, void* stream);
 
 /* Cache update K0, V0 <- K_S, V_S (Section 3).  k, v: device [B,H,L,D] with
- * the problem's strides; keep_idx: device int32 [B,H,C], each entry in
- * [0, L) (not checked on the device); k_out, v_out: device [B,H,C,D]
- * contiguous.  Bit-exact row copies. */
+ * the problem's strides; keep_idx: device int32 [B,H,C], strictly ascending
+ * per head (as nacl_select writes it); an entry outside [0, L) gives a row
+ * of zeros (no memory outside the head is read).  Two output forms:
+ *  - k_out, v_out: device [B,H,C,D] contiguous, overlapping no input;
+ *  - in place (k_out == k and v_out == v, K and V disjoint): row c of each
+ *    head takes row keep_idx[c] of the same head, in the input's own layout,
+ *    for c < C; rows C..L-1 keep their old contents.  This is the cache
+ *    update of the generation phase (Section 3, "Generation Phase Eviction"),
+ *    where the cache is a fixed buffer of L rows per head.
+ * Bit-exact row copies. */
 int nacl_compact(const nacl_problem* p, const void* k, const void* v,
                  const int32_t* keep_idx, int32_t C, void* k_out, void* v_out,
                  void* stream);
 
+/* Append of decode steps to the cache (Algorithm 1, generation phase: the
+ * new token's key and value join the cache): rows [row0, row0 + m) of every
+ * head of k, v (device [B,H,L,D] with the problem's k/v strides) take the m
+ * rows of k_new, v_new (device [B,H,m,D] contiguous, overlapping neither
+ * cache; K and V caches disjoint).  0 <= row0, row0 + m <= L.  Bit copies. */
+int nacl_append(const nacl_problem* p, void* k, void* v, int32_t row0,
+                const void* k_new, const void* v_new, int32_t m, void* stream);
+
 /* The whole step for one layer: score, select, compact on one stream
- * (Algorithm 1, encoding phase).  Arguments as above.
+ * (Algorithm 1, encoding phase).  Arguments as above; k_out, v_out may be
+ * k, v themselves (in-place compaction).  The health words of nacl_score
+ * apply: keep_idx, k_out and v_out are not valid when the call's word is
+ * non-zero.
  * Generation-phase eviction (Section 3, "Generation Phase Eviction"; the
  * Generation function of Algorithm 1) is the same call at decode shapes:
- * every m steps, with the cache holding C + m entries, pass L = C + m, the
- * current token as the only proxy (proxy_pos = {L - 1}, n_protect = 1), and
- * its query as a [B,H,1,D] tensor with q_stride[2] = 0; k_out, v_out receive
- * the C kept entries (a second buffer: they may not alias k, v).  Use a
- * different seed per eviction round so the random draws differ between
- * rounds. */
+ * the cache is a [B,H,L,D] buffer with L = C + m rows per head; after the
+ * m decoding steps appended their rows (nacl_append at row0 = C + t), call
+ * with the current token as the only proxy (proxy_pos = {L - 1},
+ * n_protect = 1), its query as a [B,H,1,D] tensor with q_stride[2] = 0, and
+ * k_out = k, v_out = v: the C kept entries move to rows 0..C-1 and the next
+ * m steps append after them.  Use a different seed per eviction round so
+ * the random draws differ between rounds. */
 int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* v,
                int32_t C, int32_t Cr, int32_t sampling, uint64_t seed, uint32_t layer,
                float* scores, int32_t* keep_idx, void* k_out, void* v_out,

@@ -5,7 +5,6 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
-#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -37,7 +36,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
 
 struct Layout {
-  size_t cnt, pos, lse, part, keys, fsum, total;
+  size_t cnt, pos, lse, part, keys, total;
   int n_chunks;
 };
 
@@ -49,7 +48,7 @@ Layout layout_of(const nacl_problem* p) {
   l.n_chunks = (p->L + nacl::kScoreMinChunkKeys - 1) / nacl::kScoreMinChunkKeys;  // most chunks any call uses
   size_t off = 0;
   l.cnt = off;
-  off += align_up((kCounterHeader + 2 * BH) * sizeof(uint32_t));  // header, per-head counters, head list
+  off += align_up((kCounterHeader + BH) * sizeof(uint32_t));  // header, per-head counters
   l.pos = off;
   off += align_up((size_t)p->P * sizeof(int32_t));
   l.lse = off;
@@ -58,9 +57,6 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up(BH * l.n_chunks * p->P * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
-  l.fsum = off;
-  if (nacl::score_fused_shape(p->dtype, p->D, p->P))
-    off += align_up(BH * nacl::kFusedReps * nacl::kFusedProxies * sizeof(uint64_t));
   l.total = off;
   return l;
 }
@@ -209,35 +205,6 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   sc.g_k1 = (uint32_t)(kd.seed >> 32);
   sc.g_layer = kd.layer;
   s.n_counter_words = kCounterHeader + BH;
-  // The single-read kernel (bf16, D = 128, 128 proxies, no caller
-  // log-sum-exp, a head's chunks within the resident work-groups) runs when
-  // built in (NACL_SCORE_FUSED) or asked for with NACL_SCORE_PATH=fused;
-  // NACL_SCORE_PATH=split always takes the two-pass kernels, and
-  // NACL_FUSED_PRESUM=1 sums every item ahead of its turn.  The variables
-  // exist for tests and measurements.
-  const char* path_env = std::getenv("NACL_SCORE_PATH");
-  const bool want_fused = path_env ? std::strcmp(path_env, "fused") == 0 : NACL_SCORE_FUSED != 0;
-  if (want_fused && !sc.lse_given && nacl::score_fused_shape(p->dtype, p->D, p->P)) {
-    const int n_chunks = (p->L + nacl::kFusedKeys - 1) / nacl::kFusedKeys;
-    const int n_vis = p->proxy_pos[p->P - 1] / nacl::kFusedKeys + 1;
-    if (n_vis <= nacl::score_fused_resident() && n_vis <= 255 * nacl::kFusedReps) {
-      const char* pre_env = std::getenv("NACL_FUSED_PRESUM");
-      sc.fused = 1;
-      sc.chunk_keys = nacl::kFusedKeys;
-      sc.n_chunks = n_chunks;
-      sc.total_items = BH * n_chunks;
-      sc.n_vis = n_vis;
-      sc.presum = pre_env && std::strcmp(pre_env, "1") == 0;
-      sc.fsums = reinterpret_cast<uint64_t*>(ws + l.fsum);
-      sc.fref = reinterpret_cast<float*>(ws + l.lse);
-      sc.done = words + 2;
-      sc.bad_n = words + 3;
-      sc.bad_list = words + kCounterHeader + BH;
-      hipError_t e = nacl::launch_score(s, stream);
-      if (e != hipSuccess) return hip_fail(e, "score kernel");
-      return NACL_OK;
-    }
-  }
   // Item size: the largest tpw whose items still number at least four per
   // resident work-group (two per CU); long items amortise the per-item Q
   // loads, partial stores and pipeline fill, too few leave a long tail.
@@ -293,20 +260,34 @@ int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr
   return NACL_OK;
 }
 
+// Compaction outputs either alias the inputs exactly (k_out == k and
+// v_out == v: in place, the kept rows move to the front of each head in the
+// input's own layout) or overlap no input at all.
 int check_compact_args(const nacl_problem* p, const void* k, const void* v, const int32_t* keep,
-                       int32_t C, const void* k_out, const void* v_out) {
+                       int32_t C, const void* k_out, const void* v_out, bool* in_place) {
+  *in_place = false;
   if (C < 0 || C > p->L) return fail(NACL_ERR_INVALID_ARG, "C must lie in [0, L] (got %d)", C);
   if (C == 0) return NACL_OK;
   if (!k || !v || !keep || !k_out || !v_out)
     return fail(NACL_ERR_INVALID_ARG, "compaction pointers must be non-NULL");
   if (!aligned16(k) || !aligned16(v) || !aligned16(k_out) || !aligned16(v_out))
     return fail(NACL_ERR_INVALID_ARG, "K, V, k_out, v_out must be 16-byte aligned");
-  const uintptr_t ob = (uintptr_t)p->B * p->H * C * p->D * elt_bytes(p->dtype);
   uintptr_t k0, k1, v0, v1;
   extent(k, p->k_stride, p, k0, k1);
   extent(v, p->v_stride, p, v0, v1);
-  const uintptr_t ko = (uintptr_t)k_out, vo = (uintptr_t)v_out;
   const uintptr_t kk0 = (uintptr_t)keep, kk1 = kk0 + (uintptr_t)p->B * p->H * C * 4;
+  if (overlaps(kk0, kk1, k0, k1) || overlaps(kk0, kk1, v0, v1))
+    return fail(NACL_ERR_INVALID_ARG, "keep_idx overlaps K or V");
+  if (k_out == k || v_out == v) {
+    if (k_out != k || v_out != v)
+      return fail(NACL_ERR_INVALID_ARG, "in-place compaction needs k_out == k and v_out == v");
+    if (overlaps(k0, k1, v0, v1))
+      return fail(NACL_ERR_INVALID_ARG, "in-place compaction needs K and V in disjoint memory");
+    *in_place = true;
+    return NACL_OK;
+  }
+  const uintptr_t ob = (uintptr_t)p->B * p->H * C * p->D * elt_bytes(p->dtype);
+  const uintptr_t ko = (uintptr_t)k_out, vo = (uintptr_t)v_out;
   if (overlaps(ko, ko + ob, k0, k1) || overlaps(ko, ko + ob, v0, v1) || overlaps(vo, vo + ob, k0, k1) ||
       overlaps(vo, vo + ob, v0, v1) || overlaps(ko, ko + ob, vo, vo + ob) ||
       overlaps(ko, ko + ob, kk0, kk1) || overlaps(vo, vo + ob, kk0, kk1))
@@ -315,12 +296,13 @@ int check_compact_args(const nacl_problem* p, const void* k, const void* v, cons
 }
 
 int run_compact(const nacl_problem* p, const void* k, const void* v, const int32_t* keep, int32_t C,
-                void* k_out, void* v_out, hipStream_t stream) {
+                void* k_out, void* v_out, bool in_place, uint32_t* health, hipStream_t stream) {
   if (C == 0) return NACL_OK;
   nacl::CompactLaunch c{};
   const int eb = elt_bytes(p->dtype);
   c.B = p->B;
   c.H = p->H;
+  c.L = p->L;
   c.C = C;
   c.row_vecs = p->D * eb / 16;
   for (int i = 0; i < 3; ++i) {
@@ -332,6 +314,8 @@ int run_compact(const nacl_problem* p, const void* k, const void* v, const int32
   c.keep = keep;
   c.k_out = k_out;
   c.v_out = v_out;
+  c.in_place = in_place ? 1 : 0;
+  c.health = health;
   hipError_t e = nacl::launch_compact(c, stream);
   if (e != hipSuccess) return hip_fail(e, "compact kernel");
   return NACL_OK;
@@ -384,8 +368,48 @@ int nacl_compact(const nacl_problem* p, const void* k, const void* v, const int3
   g_detail[0] = 0;
   int st = check_problem(p);
   if (st) return st;
-  if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out))) return st;
-  return run_compact(p, k, v, keep_idx, C, k_out, v_out, static_cast<hipStream_t>(stream));
+  bool in_place = false;
+  if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out, &in_place))) return st;
+  return run_compact(p, k, v, keep_idx, C, k_out, v_out, in_place, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int nacl_append(const nacl_problem* p, void* k, void* v, int32_t row0, const void* k_new,
+                const void* v_new, int32_t m, void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if (m < 0 || row0 < 0 || (int64_t)row0 + m > p->L)
+    return fail(NACL_ERR_INVALID_ARG, "rows [%d, %lld) must lie in [0, L = %d)", row0, (long long)row0 + m, p->L);
+  if (m == 0) return NACL_OK;
+  if (!k || !v || !k_new || !v_new) return fail(NACL_ERR_INVALID_ARG, "append pointers must be non-NULL");
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_new) || !aligned16(v_new))
+    return fail(NACL_ERR_INVALID_ARG, "K, V, k_new, v_new must be 16-byte aligned");
+  uintptr_t k0, k1, v0, v1;
+  extent(k, p->k_stride, p, k0, k1);
+  extent(v, p->v_stride, p, v0, v1);
+  const uintptr_t nb = (uintptr_t)p->B * p->H * m * p->D * elt_bytes(p->dtype);
+  const uintptr_t kn = (uintptr_t)k_new, vn = (uintptr_t)v_new;
+  if (overlaps(kn, kn + nb, k0, k1) || overlaps(kn, kn + nb, v0, v1) || overlaps(vn, vn + nb, k0, k1) ||
+      overlaps(vn, vn + nb, v0, v1) || overlaps(k0, k1, v0, v1))
+    return fail(NACL_ERR_INVALID_ARG, "k_new / v_new overlap the cache, or K overlaps V");
+  nacl::AppendLaunch a{};
+  const int eb = elt_bytes(p->dtype);
+  a.B = p->B;
+  a.H = p->H;
+  a.row0 = row0;
+  a.m = m;
+  a.row_vecs = p->D * eb / 16;
+  for (int i = 0; i < 3; ++i) {
+    a.ks[i] = p->k_stride[i] * eb / 16;
+    a.vs[i] = p->v_stride[i] * eb / 16;
+  }
+  a.k = k;
+  a.v = v;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  hipError_t e = nacl::launch_append(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "append kernel");
+  return NACL_OK;
 }
 
 int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* v, int32_t C,
@@ -399,7 +423,8 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
   if (!q || !scores) return fail(NACL_ERR_INVALID_ARG, "q and scores must be non-NULL");
   if (!aligned16(q)) return fail(NACL_ERR_INVALID_ARG, "q must be 16-byte aligned");
   if (C > 0 && !keep_idx) return fail(NACL_ERR_INVALID_ARG, "keep_idx must be non-NULL");
-  if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out))) return st;
+  bool in_place = false;
+  if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out, &in_place))) return st;
   if (!k) return fail(NACL_ERR_INVALID_ARG, "k must be non-NULL");
   if ((st = check_ws(p, ws, ws_bytes))) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -416,7 +441,8 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
   kd.layer = layer;
   if ((st = run_score(p, q, k, nullptr, scores, w, l, pos_dev, s, kd))) return st;
   if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s, kd.on))) return st;
-  return run_compact(p, k, v, keep_idx, C, k_out, v_out, s);
+  uint32_t* health = reinterpret_cast<uint32_t*>(w + l.cnt) + 1;
+  return run_compact(p, k, v, keep_idx, C, k_out, v_out, in_place, health, s);
 }
 
 const char* nacl_status_string(int status) {

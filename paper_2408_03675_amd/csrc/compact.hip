@@ -4,6 +4,11 @@
 // sides are coalesced.  K and V rows go to separate blocks (blockIdx.z), and
 // with no loop every thread's load is in flight from its first instruction;
 // many small blocks keep the whole chip issuing.  Rows are bit copies.
+//
+// Also here: the in-place form of the same update for a decode-time cache
+// (Section 3, generation-phase eviction: the kept rows move to the front of
+// each head's own rows), and the append of new decode steps' rows to the
+// cache (Algorithm 1, generation phase).
 
 #include "device_common.h"
 #include "internal.h"
@@ -11,6 +16,15 @@
 namespace nacl {
 
 constexpr int kCompactThreads = 512;
+
+// A keep index outside [0, L) gives a zero row and sets bit 2 of the health
+// words (when the launch has them) instead of reading outside the head.
+__device__ __forceinline__ void flag_bad_index(uint32_t* health) {
+  if (health) {
+    atomicOr(health, 4u);
+    atomicOr(health + 1, 4u);
+  }
+}
 
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(CompactLaunch a) {
   const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
@@ -20,18 +34,100 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(CompactLaunch 
   const int vec = threadIdx.x % vpr;
   const bool is_v = blockIdx.z != 0;
   const int64_t* st = is_v ? a.vs : a.ks;
-  const int64_t j = a.keep[(int64_t)bh * a.C + r];
-  const u32x4* src = static_cast<const u32x4*>(is_v ? a.v : a.k) + b * st[0] + h * st[1] + j * st[2] + vec;
+  const int j = a.keep[(int64_t)bh * a.C + r];
+  u32x4 x = u32x4{0u, 0u, 0u, 0u};
+  if ((unsigned)j < (unsigned)a.L) {
+    const u32x4* src = static_cast<const u32x4*>(is_v ? a.v : a.k) + b * st[0] + h * st[1] + j * st[2] + vec;
+    x = __builtin_nontemporal_load(src);
+  } else if (vec == 0) {
+    flag_bad_index(a.health);
+  }
   u32x4* dst = static_cast<u32x4*>(is_v ? a.v_out : a.k_out) + ((int64_t)bh * a.C + r) * vpr + vec;
-  __builtin_nontemporal_store(__builtin_nontemporal_load(src), dst);
+  __builtin_nontemporal_store(x, dst);
+}
+
+// In place: row c of each head takes row keep[c] of the same head, in the
+// input's own layout.  keep is strictly ascending, so keep[c] >= c and the
+// rows a chunk of destinations [c0, c1) reads lie at or after c0: rows that
+// no earlier chunk writes.  One work-group per (head, K or V) walks the
+// chunks in order; inside a chunk every source is read (the barrier waits
+// for the loads) before any destination is written, since a source of one
+// row may be the destination of another row of the same chunk.  Rows with
+// keep[c] == c stay where they are.
+constexpr int kInplaceThreads = 1024;
+constexpr int kInplaceVecs = 4;  // vectors per thread and chunk
+
+__global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(CompactLaunch a) {
+  const int bh = blockIdx.x, b = bh / a.H, h = bh % a.H;
+  const bool is_v = blockIdx.y != 0;
+  const int64_t* st = is_v ? a.vs : a.ks;
+  u32x4* base = static_cast<u32x4*>(is_v ? a.v_out : a.k_out) + b * st[0] + h * st[1];
+  const int vpr = a.row_vecs;
+  const int rows_per_chunk = kInplaceThreads * kInplaceVecs / vpr;
+  const int32_t* keep = a.keep + (int64_t)bh * a.C;
+  for (int c0 = 0; c0 < a.C; c0 += rows_per_chunk) {
+    u32x4 x[kInplaceVecs];
+    int dst[kInplaceVecs];
+#pragma unroll
+    for (int u = 0; u < kInplaceVecs; ++u) {
+      const int idx = u * kInplaceThreads + (int)threadIdx.x;
+      const int r = c0 + idx / vpr, vec = idx % vpr;
+      dst[u] = -1;
+      x[u] = u32x4{0u, 0u, 0u, 0u};
+      if (r < a.C) {
+        const int j = keep[r];
+        if ((unsigned)j >= (unsigned)a.L) {
+          dst[u] = r;  // zero row
+          if (vec == 0) flag_bad_index(a.health);
+        } else if (j != r) {
+          x[u] = base[(int64_t)j * st[2] + vec];
+          dst[u] = r;
+        }
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kInplaceVecs; ++u) {
+      const int idx = u * kInplaceThreads + (int)threadIdx.x;
+      if (dst[u] >= 0) base[(int64_t)dst[u] * st[2] + idx % vpr] = x[u];
+    }
+  }
+}
+
+// Append: rows [row0, row0 + m) of every head of the cache take the m rows
+// of k_new / v_new ([B, H, m, D] contiguous).
+__global__ __launch_bounds__(kCompactThreads) void append_kernel(AppendLaunch a) {
+  const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  const int vpr = a.row_vecs;
+  const int r = blockIdx.x * (kCompactThreads / vpr) + (int)threadIdx.x / vpr;
+  if (r >= a.m) return;
+  const int vec = threadIdx.x % vpr;
+  const bool is_v = blockIdx.z != 0;
+  const int64_t* st = is_v ? a.vs : a.ks;
+  const u32x4* src = static_cast<const u32x4*>(is_v ? a.v_new : a.k_new) + ((int64_t)bh * a.m + r) * vpr + vec;
+  u32x4* dst = static_cast<u32x4*>(is_v ? a.v : a.k) + b * st[0] + h * st[1] + (int64_t)(a.row0 + r) * st[2] + vec;
+  *dst = *src;
 }
 
 hipError_t launch_compact(const CompactLaunch& a, hipStream_t stream) {
   if (a.C == 0) return hipSuccess;
   if (a.row_vecs <= 0 || kCompactThreads % a.row_vecs != 0) return hipErrorInvalidValue;
+  if (a.in_place) {
+    hipLaunchKernelGGL(compact_inplace_kernel, dim3(a.B * a.H, 2), dim3(kInplaceThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   const int rows_per_block = kCompactThreads / a.row_vecs;
   dim3 grid((a.C + rows_per_block - 1) / rows_per_block, a.B * a.H, 2);
   hipLaunchKernelGGL(compact_kernel, grid, dim3(kCompactThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendLaunch& a, hipStream_t stream) {
+  if (a.m == 0) return hipSuccess;
+  if (a.row_vecs <= 0 || kCompactThreads % a.row_vecs != 0) return hipErrorInvalidValue;
+  const int rows_per_block = kCompactThreads / a.row_vecs;
+  dim3 grid((a.m + rows_per_block - 1) / rows_per_block, a.B * a.H, 2);
+  hipLaunchKernelGGL(append_kernel, grid, dim3(kCompactThreads), 0, stream, a);
   return hipGetLastError();
 }
 

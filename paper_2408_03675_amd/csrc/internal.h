@@ -44,23 +44,6 @@ constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter o
 #endif
 constexpr int kSplitChunkKeys = NACL_SPLIT_CHUNK;
 inline bool score_uses_split(int dtype, int D, int P) { return NACL_SCORE_SPLIT && dtype == 1 && D == 128 && P >= 128; }
-// Single-read variant (bf16, D = 128, exactly 128 proxies, log-sum-exp not
-// given): items of kFusedKeys keys whose exponentials stay in registers
-// until the head's row sums are complete, so K is read once.  Off by default
-// (slower than the two-pass proxy-split kernel on MI355X, see score.hip);
-// NACL_SCORE_PATH=fused in the environment selects it per call.
-#ifndef NACL_SCORE_FUSED
-#define NACL_SCORE_FUSED 0
-#endif
-constexpr int kFusedKeys = 128;
-constexpr int kFusedProxies = 128;
-#ifndef NACL_FUSED_REPS
-#define NACL_FUSED_REPS 4
-#endif
-constexpr int kFusedReps = NACL_FUSED_REPS;  // replicas of each head's row-sum words
-inline bool score_fused_shape(int dtype, int D, int P) { return dtype == 1 && D == 128 && P == kFusedProxies; }
-// Resident work-groups of the single-read kernel on the current device (0 on error).
-int score_fused_resident();
 // The workspace is sized for the shortest item of either kernel.
 constexpr int kScoreMinChunkKeys = std::min(kScoreTpwMin * kScoreWaves * 16, kSplitChunkKeys);
 
@@ -83,7 +66,8 @@ struct ScoreSched {
   int total_items;
   int lse_given;         // 1: the caller supplied the log-sum-exp, only pass 2 runs
   uint32_t* queue;       // workspace counter words: queue, status, then per-head counters
-  uint32_t* status;      // bit 0 set if a pass-2 wait hit its spin limit (never expected)
+  uint32_t* status;      // health words: [0] this call's, [1] sticky; bit 0 set if a pass-2
+                         // wait hit its spin limit (never expected)
   uint32_t* head_cnt;    // [B*H]
   float2* partials;      // [B*H, n_chunks, P] base-2 (max, sum)
   float* lse2;           // [B*H, P] base-2 log-sum-exp
@@ -96,15 +80,6 @@ struct ScoreSched {
   uint32_t* gkeys;       // [B*H, L]
   int g_mode;
   uint32_t g_k0, g_k1, g_layer;
-  // Single-read kernel only (see score.hip).
-  int fused;             // 1: run score_fused_kernel
-  int n_vis;             // chunks per head that start at or before the last proxy
-  int presum;            // 1: sum every item ahead of its turn (exercises the ahead-of-turn path)
-  uint64_t* fsums;       // [B*H, kFusedReps, 128] fixed-point row sums with arrival counts
-  float* fref;           // [B*H, 128] base-2 reference of each proxy row
-  uint32_t* done;        // work-groups that finished their items
-  uint32_t* bad_n;       // heads on bad_list
-  uint32_t* bad_list;    // [B*H] heads whose row sums left the fixed-point range
 };
 
 struct ScoreLaunch {
@@ -133,15 +108,28 @@ hipError_t launch_select(const SelectLaunch& L, hipStream_t stream);
 size_t select_lds_bytes(int L);
 
 struct CompactLaunch {
-  int B, H, C, row_vecs;        // row_vecs = D * elt / 16
+  int B, H, L, C, row_vecs;     // row_vecs = D * elt / 16
   int64_t ks[3], vs[3];         // strides in 16-byte units
   const void* k;
   const void* v;
   const int32_t* keep;
-  void* k_out;
-  void* v_out;
+  void* k_out;                  // == k when in_place
+  void* v_out;                  // == v when in_place
+  int in_place;                 // 1: rows 0..C-1 of each head of k, v take the kept rows
+  uint32_t* health;             // health words (call's, sticky) or nullptr
 };
 
 hipError_t launch_compact(const CompactLaunch& L, hipStream_t stream);
+
+struct AppendLaunch {
+  int B, H, row0, m, row_vecs;
+  int64_t ks[3], vs[3];         // cache strides in 16-byte units
+  void* k;
+  void* v;
+  const void* k_new;            // [B, H, m, D] contiguous
+  const void* v_new;
+};
+
+hipError_t launch_append(const AppendLaunch& L, hipStream_t stream);
 
 }  // namespace nacl

@@ -639,6 +639,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
             __builtin_amdgcn_s_sleep(2);
             if (++spins > kSpinLimit) {
               atomicOr(s.status, 1u);
+              atomicOr(s.status + 1, 1u);
               break;
             }
           }
@@ -726,9 +727,11 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
   }
 }
 
-// Zeroes the queue counter, the per-head counters and the status word.
+// Zeroes the queue counter, the call's health word and the per-head
+// counters; the sticky health word (word 2) is left as it is.
 __global__ void score_init_kernel(uint32_t* words, int n) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) words[i] = 0u;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+    if (i != 2) words[i] = 0u;
 }
 
 // ---------------------------------------------------------------------------
@@ -1067,6 +1070,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
             __builtin_amdgcn_s_sleep(2);
             if (++spins > kSpinLimit) {
               atomicOr(s.status, 1u);
+              atomicOr(s.status + 1, 1u);
               break;
             }
           }
@@ -1170,569 +1174,6 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
 }
 
 // ---------------------------------------------------------------------------
-// Single-read variant: bf16, D = 128, exactly 128 proxies, log-sum-exp not
-// given.  The two-pass kernels above read K twice because the column
-// reduction of a chunk needs the log-sum-exp of every proxy row, i.e. the
-// whole head's first pass.  This kernel keeps what the second pass needs in
-// registers instead: an item is kFusedKeys keys, and its pass-1 values
-// E = exp2(logit * c2 - R) (R: a fixed base-2 reference per proxy row and
-// head, the row's maximum over keys 0..15, which every proxy sees) stay in
-// the waves' VGPRs.  Since every item of a head uses the same reference, the
-// row sums of the items simply add up: each item adds its row sums, rounded
-// to a fixed-point integer, to the head's 64-bit sum words with one atomic
-// add per row.  Integer addition is associative, so the totals do not depend
-// on the arrival order and the scores stay bit-reproducible.  Each word also
-// counts its additions in its low 8 bits, so a reader knows from the word
-// itself whether every item of the head has arrived; no separate flag or
-// fence is needed.  Once a head's words are complete, F[j] = sum_i E_ij / l_i
-// where l_i is the row's total (then exp2(R - LSE) = 1 / l).
-//
-// Pipeline per work-group (4 waves, each with 32 proxies and 64 VGPRs of E
-// per item): items are taken from a ticket counter in head-major order; an
-// item's E stays live for one further item, so the column reduction of item
-// n runs after the first pass of item n + 1 and normally finds its head
-// complete.  K tiles of the next item are loaded into LDS (one of two 32 KB
-// buffers) while the current item waits and reduces.  Wave 0 issues no K
-// loads; it takes tickets, reads the sum words and writes F, so its memory
-// waits never wait on K.  Wave 1 adds the row sums (fire and forget).
-//
-// Progress: before a work-group waits for head h it holds two items whose
-// sums are in (or in earlier heads), and any item it has taken but not yet
-// summed that belongs to h is summed first (ahead of its turn, without
-// keeping E; its E is recomputed from LDS at its turn).  So a wait never
-// depends on the waiting group itself, and the items a waiting group holds
-// are older than everything not yet taken: with W resident work-groups all
-// waiting on h, h would own 2 W summed items, which is more than its chunks
-// whenever 2 W > chunks per head.  The launcher requires W >= chunks per
-// head.
-//
-// Range: an item adds at most 2^23 (row sum relative to R) per row; sums are
-// in units of 2^-24 above the 8 count bits, so up to 255 items per word
-// (kFusedReps words per row, item c adding to word c mod kFusedReps) never
-// carry into the count's neighbour or into bit 63.  An item whose row sum exceeds that (a key far
-// above keys 0..15 for some proxy) poisons the head (bit 63 of its words):
-// its items skip the column reduction, and the last work-group to finish
-// recomputes such heads with an exact three-sweep path.
-constexpr int kFusedTiles = kFusedKeys / 16;
-constexpr float kFusedUnit = 16777216.f;      // 2^24 fixed-point units per 1.0
-constexpr float kFusedItemMax = 8388608.f;    // 2^23: largest row sum one item may add
-constexpr uint64_t kFusedPoison = 1ull << 63;
-constexpr uint64_t kFusedRawMask = (1ull << 55) - 1;  // sum field: bits 8 .. 62
-constexpr uint32_t kFusedSpinLimit = 1u << 20;
-
-__device__ __forceinline__ uint64_t load_coherent64(const uint64_t* p) {
-  return __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float row_sum16(float v) {  // sum over the 16 key lanes of a lane group
-  v += __shfl_xor(v, 1);
-  v += __shfl_xor(v, 2);
-  v += __shfl_xor(v, 4);
-  return v + __shfl_xor(v, 8);
-}
-__device__ __forceinline__ float row_max16(float v) {
-  v = fmaxf(v, __shfl_xor(v, 1));
-  v = fmaxf(v, __shfl_xor(v, 2));
-  v = fmaxf(v, __shfl_xor(v, 4));
-  return fmaxf(v, __shfl_xor(v, 8));
-}
-
-// Zeroes the counter words and every head's sum words, and computes the
-// heads' references R (one work-group per head, the same MFMA sequence as
-// the main kernel's first tile, so R is bit-identical to what chunk 0 sees).
-__global__ __launch_bounds__(kScoreThreads) void score_fused_init_kernel(const __bf16* __restrict__ q,
-                                                                         const __bf16* __restrict__ k, ScoreArgs a,
-                                                                         ScoreSched s, int n_words) {
-  using M = Mma<__bf16, 128>;
-  using frag_t = typename M::frag_t;
-  constexpr int kS = M::kSteps;
-  const int bh = blockIdx.x;
-  for (int i = bh * kScoreThreads + threadIdx.x; i < n_words; i += gridDim.x * kScoreThreads) s.queue[i] = 0u;
-  uint64_t* sw = s.fsums + (int64_t)bh * kFusedReps * kFusedProxies;
-  for (int i = threadIdx.x; i < kFusedReps * kFusedProxies; i += kScoreThreads) sw[i] = 0ull;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r16 = lane & 15, g = lane >> 4, w0 = 32 * wave;
-  const int b = bh / a.H, h = bh % a.H;
-  const __bf16* qb = q + b * a.qs[0] + h * a.qs[1];
-  const __bf16* kb = k + b * a.ks[0] + h * a.ks[1];
-  const uint32_t row_bytes = (uint32_t)(a.ks[2] * 2);
-  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<__bf16*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + 256u), kBufferRsrcWord3);
-  frag_t kf[kS];
-  M::load_k(rsrc, (uint32_t)r16 * row_bytes + 16u * (uint32_t)g, kf);
-#pragma unroll
-  for (int pb = 0; pb < 2; ++pb) {
-    frag_t qf[kS];
-    M::load(qb + (int64_t)a.pos[w0 + 16 * pb + r16] * a.qs[2], g, qf);
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < kS; ++ks) acc = M::mma(qf[ks], kf[ks], acc);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int i = w0 + 16 * pb + 4 * g + e;
-      const float m = row_max16(r16 <= a.pos[i] ? acc[e] : -INFINITY);
-      if (r16 == 0) s.fref[(int64_t)bh * kFusedProxies + i] = m * a.c2;
-    }
-  }
-}
-
-__global__ __launch_bounds__(kScoreThreads, 2) void score_fused_kernel(const __bf16* __restrict__ q,
-                                                                      const __bf16* __restrict__ k, ScoreArgs a,
-                                                                      ScoreSched s) {
-  using T = __bf16;
-  constexpr int D = 128;
-  using M = Mma<T, D>;
-  using KS = KStage<T, D>;
-  using frag_t = typename M::frag_t;
-  constexpr int kS = M::kSteps;
-  constexpr int kTB = KS::kTileBytes;
-  typedef f32x4 EBuf[kFusedTiles][2];
-  __shared__ int pos_s[kFusedProxies];
-  __shared__ __attribute__((aligned(16))) unsigned char kbuf0[kFusedTiles * kTB];
-  __shared__ __attribute__((aligned(16))) unsigned char kbuf1[kFusedTiles * kTB];
-  __shared__ __attribute__((aligned(16))) float stage_s[kScoreWaves][kFusedKeys];
-  __shared__ float rows_s[kFusedProxies];
-  __shared__ __attribute__((aligned(16))) float w_s[kFusedProxies];
-  __shared__ float fcol_s[kFusedKeys];
-  __shared__ int tick_s, state_s, last_s;
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int r16 = lane & 15, g = lane >> 4;
-  const int w0 = 32 * wave;
-  const float c2 = a.c2;
-  const uint32_t row_bytes = (uint32_t)(a.ks[2] * (int64_t)sizeof(T));
-  uint32_t vo_all[KS::kInstr];
-  KS::offsets(row_bytes, lane, vo_all);
-  const int first_w = __builtin_amdgcn_readfirstlane(a.pos[w0]);
-  const int last_w = __builtin_amdgcn_readfirstlane(a.pos[w0 + 31]);
-  for (int i = threadIdx.x; i < kFusedProxies; i += kScoreThreads) pos_s[i] = a.pos[i];
-
-  auto head_of = [&](int t) { return t / s.n_chunks; };
-  auto key0_of = [&](int t) { return (t % s.n_chunks) * kFusedKeys; };
-  auto beyond = [&](int t) { return key0_of(t) > a.p_last; };
-  auto rsrc_of = [&](int bh) {
-    const T* kb = k + (bh / a.H) * a.ks[0] + (bh % a.H) * a.ks[1];
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kb), (short)0,
-                                             (int)((uint32_t)(a.L - 1) * row_bytes + (uint32_t)(D * sizeof(T))),
-                                             kBufferRsrcWord3);
-  };
-  // Waves 1..3 load the item's 8 tiles (32 DMA instructions of 1 KB) into buf.
-  auto dma = [&](int t, unsigned char* buf) {
-    if (wave == 0) return;
-    const __amdgpu_buffer_rsrc_t rs = rsrc_of(head_of(t));
-    const uint32_t base = (uint32_t)key0_of(t) * row_bytes;
-    for (int i = wave - 1; i < KS::kInstr * kFusedTiles; i += kScoreWaves - 1) {
-      const int tt = i / KS::kInstr, part = i % KS::kInstr;
-      uint32_t vo = vo_all[0];
-#pragma unroll
-      for (int j = 1; j < KS::kInstr; ++j) vo = part == j ? vo_all[j] : vo;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(buf + tt * kTB + part * 1024),
-                                               16, vo + base + (uint32_t)(16 * tt) * row_bytes, 0, 0, kScoreKAux);
-    }
-  };
-  auto load_q = [&](int bh, frag_t (&qf)[2][kS], f32x4 (&rr)[2]) {
-    const T* qb = q + (bh / a.H) * a.qs[0] + (bh % a.H) * a.qs[1];
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
-      M::load(qb + (int64_t)pos_s[w0 + 16 * pb + r16] * a.qs[2], g, qf[pb]);
-      rr[pb] = *reinterpret_cast<const f32x4*>(s.fref + (int64_t)bh * kFusedProxies + w0 + 16 * pb + 4 * g);
-    }
-  };
-  // Pass 1 over the item in buf: KEEP stores E, SUM accumulates row sums.
-  auto pass1 = [&](const unsigned char* buf, int key0c, const frag_t (&qf)[2][kS], const f32x4 (&rr)[2], EBuf& E,
-                   float (&ls)[2][4], auto keep_c, auto sum_c) __attribute__((always_inline)) {
-    constexpr bool KEEP = decltype(keep_c)::value;
-    constexpr bool SUM = decltype(sum_c)::value;
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) ls[pb][e] = 0.f;
-    static_for<kFusedTiles>([&](auto t_c) {
-      constexpr int t = decltype(t_c)::value;
-      const int key0 = key0c + 16 * t;
-      if (key0 > last_w) {
-        if constexpr (KEEP) {
-          E[t][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-          E[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-        return;
-      }
-      frag_t kf[kS];
-      KS::template frag<M>(buf + t * kTB, r16, g, kf);
-      const bool full = key0 + 15 <= first_w;
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
-        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < kS; ++ks) acc = M::mma(qf[pb][ks], kf[ks], acc);
-        f32x4 x;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x[e] = fast_exp2(fmaf(acc[e], c2, -rr[pb][e]));
-        if (!full) {
-          const int* pl = pos_s + w0 + 16 * pb + opaque(4 * g);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) x[e] = key0 + r16 <= pl[e] ? x[e] : 0.f;
-        }
-        if constexpr (KEEP) E[t][pb] = x;
-        if constexpr (SUM) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) ls[pb][e] += x[e];
-        }
-      }
-    });
-  };
-  // Adds the item's row sums to its head's words (wave 1, which waits on
-  // nothing else; fire and forget).
-  auto arrive = [&](int t, float (&ls)[2][4]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float v = row_sum16(ls[pb][e]);
-        if (r16 == 0) rows_s[w0 + 16 * pb + 4 * g + e] = v;
-      }
-    __syncthreads();
-    if (wave == 1) {
-      const int bh = head_of(t), c = t % s.n_chunks;
-      uint64_t* sw = s.fsums + ((int64_t)bh * kFusedReps + c % kFusedReps) * kFusedProxies;
-      const float l0 = rows_s[lane], l1 = rows_s[lane + 64];
-      const bool ok = l0 < kFusedItemMax && l1 < kFusedItemMax;  // false for NaN
-      if (__builtin_amdgcn_ballot_w64(!ok) == 0) {
-        const uint64_t v0 = ((uint64_t)(l0 * kFusedUnit) << 8) | 1ull;
-        const uint64_t v1 = ((uint64_t)(l1 * kFusedUnit) << 8) | 1ull;
-        __hip_atomic_fetch_add(sw + lane, v0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(sw + lane + 64, v1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      } else {
-        if (lane == 0) {
-          if (atomicOr(&s.head_cnt[bh], 1u) == 0u) {
-            const uint32_t idx = atomicAdd(s.bad_n, 1u);
-            __hip_atomic_store(s.bad_list + idx, (uint32_t)bh, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
-        }
-        __hip_atomic_fetch_or(sw + lane, kFusedPoison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_or(sw + lane + 64, kFusedPoison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        wait_stores();
-        __hip_atomic_fetch_add(sw + lane, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(sw + lane + 64, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-  };
-  // Wave 0: 0 = the head's sums are incomplete, 1 = complete (w_s holds
-  // 1 / l per proxy), 2 = poisoned.
-  auto poll_issue = [&](int bh, uint64_t (&v)[2][kFusedReps]) {
-    const uint64_t* sw = s.fsums + (int64_t)bh * kFusedReps * kFusedProxies;
-#pragma unroll
-    for (int r = 0; r < kFusedReps; ++r) {
-      v[0][r] = load_coherent64(sw + r * kFusedProxies + lane);
-      v[1][r] = load_coherent64(sw + r * kFusedProxies + lane + 64);
-    }
-  };
-  auto poll_finish = [&](const uint64_t (&v)[2][kFusedReps]) -> int {
-    bool complete = true, poisoned = false;
-    float w[2];
-#pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      uint32_t cnt = 0;
-      uint64_t raw = 0;
-#pragma unroll
-      for (int r = 0; r < kFusedReps; ++r) {
-        cnt += (uint32_t)(v[hh][r] & 255ull);
-        raw += (v[hh][r] >> 8) & kFusedRawMask;
-        poisoned |= (v[hh][r] & kFusedPoison) != 0;
-      }
-      complete &= cnt == (uint32_t)s.n_vis;
-      w[hh] = (float)(1.0 / ((double)raw * (1.0 / 16777216.0)));
-    }
-    if (__builtin_amdgcn_ballot_w64(!complete) != 0) return 0;
-    if (__builtin_amdgcn_ballot_w64(poisoned) != 0) return 2;
-    w_s[lane] = w[0];
-    w_s[lane + 64] = w[1];
-    return 1;
-  };
-  // Column sums of an item from its E and w_s; wave 0 writes F (and the
-  // Gumbel keys).
-  auto pass2 = [&](int t, const EBuf& E) __attribute__((always_inline)) {
-    const int bh = head_of(t), key0c = key0_of(t);
-    f32x4 wv[2];
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb) wv[pb] = *reinterpret_cast<const f32x4*>(w_s + w0 + 16 * pb + 4 * g);
-    float cs[kFusedTiles];
-#pragma unroll
-    for (int tt = 0; tt < kFusedTiles; ++tt) {
-      float x = 0.f;
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x = fmaf(E[tt][pb][e], wv[pb][e], x);
-      cs[tt] = x;
-    }
-#pragma unroll
-    for (int t0 = 0; t0 < kFusedTiles; t0 += 4)
-      stage_s[wave][(t0 + g) * 16 + r16] = colsum4(cs[t0], cs[t0 + 1], cs[t0 + 2], cs[t0 + 3]);
-    __syncthreads();
-    if (wave == 0) {
-      float* F = s.scores + (int64_t)bh * a.L;
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        const int idx = lane + 64 * hh;
-        const float f = ((stage_s[0][idx] + stage_s[1][idx]) + stage_s[2][idx]) + stage_s[3][idx];
-        if (key0c + idx < a.L) F[key0c + idx] = f;
-        fcol_s[idx] = f;
-      }
-      if (s.gkeys) {
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        const int j0 = key0c + 4 * lane;
-        if (lane < kFusedKeys / 4 && j0 < a.L) {
-          const int n = min(4, a.L - j0);
-          float fv[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) fv[e] = fcol_s[4 * lane + e];
-          uint32_t kv[4];
-          gumbel_block_keys(s.g_mode, j0, n, bh / a.H, bh % a.H, s.g_layer, s.g_k0, s.g_k1, fv, kv);
-          uint32_t* gk = s.gkeys + (int64_t)bh * a.L;
-          for (int e = 0; e < n; ++e) gk[j0 + e] = kv[e];
-        }
-      }
-    }
-  };
-  // Items past the last proxy: zeros.
-  auto zero_item = [&](int t) {
-    if (wave != 0) return;
-    const int bh = head_of(t), key0c = key0_of(t);
-    float* F = s.scores + (int64_t)bh * a.L;
-    for (int idx = lane; idx < kFusedKeys; idx += 64)
-      if (key0c + idx < a.L) F[key0c + idx] = 0.f;
-    if (s.gkeys) {
-      const int j0 = key0c + 4 * lane;
-      if (lane < kFusedKeys / 4 && j0 < a.L) {
-        const int n = min(4, a.L - j0);
-        float fv[4] = {0.f, 0.f, 0.f, 0.f};
-        uint32_t kv[4];
-        gumbel_block_keys(s.g_mode, j0, n, bh / a.H, bh % a.H, s.g_layer, s.g_k0, s.g_k1, fv, kv);
-        uint32_t* gk = s.gkeys + (int64_t)bh * a.L;
-        for (int e = 0; e < n; ++e) gk[j0 + e] = kv[e];
-      }
-    }
-  };
-
-  // Pipeline state (block-uniform): itA and itB have their sums in (E in Ea and
-  // Eb), itC is the next item (ticket taken; its K possibly loading), itD the
-  // one after.
-  int itA = -1, itB = -1, itC = -1, itD = -1;
-  bool c_dma = false, c_pre = false, d_dma = false, d_pre = false;
-  bool c_q = false;  // Q and R of itC already in qf / rr
-  int c_buf = 0;
-  frag_t qf[2][kS];
-  f32x4 rr[2];
-  EBuf E0, E1;
-  if (threadIdx.x == 0) tick_s = (int)atomicAdd(s.queue, 1u);
-  __syncthreads();
-  itC = tick_s < s.total_items ? tick_s : -1;
-
-  auto body = [&](EBuf& Ea) __attribute__((always_inline)) -> bool {
-    unsigned char* cb = c_buf ? kbuf1 : kbuf0;
-    unsigned char* db = c_buf ? kbuf0 : kbuf1;
-    const bool c_real = itC >= 0 && !beyond(itC);
-    if (c_real) {
-      if (!c_dma) dma(itC, cb);
-      c_dma = true;
-      if (!c_q) load_q(head_of(itC), qf, rr);
-    }
-    // Wave 0: the ticket after itC and the state of itA's head.
-    if (wave == 0) {
-      uint32_t tk = 0xFFFFFFFFu;
-      if (lane == 0 && itC >= 0) tk = atomicAdd(s.queue, 1u);
-      uint64_t v[2][kFusedReps];
-      if (itA >= 0) poll_issue(head_of(itA), v);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      const int st = itA >= 0 ? poll_finish(v) : 1;
-      if (lane == 0) {
-        tick_s = (int)tk;
-        state_s = st;
-      }
-    }
-    __syncthreads();
-    itD = (itC >= 0 && (uint32_t)tick_s < (uint32_t)s.total_items) ? tick_s : -1;
-    int st = state_s;
-    bool q_dirty = false;
-    if (itA >= 0 && (st == 0 || s.presum)) {
-      // Sum, ahead of their turn, the items taken but not summed that belong
-      // to itA's head (with presum: all of them), then wait.
-      auto presum = [&](int X, unsigned char* xb, bool& x_dma) __attribute__((always_inline)) {
-        if (!x_dma) dma(X, xb);
-        x_dma = true;
-        load_q(head_of(X), qf, rr);
-        q_dirty = true;
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __syncthreads();
-        float ls[2][4];
-        pass1(xb, key0_of(X), qf, rr, Ea, ls, std::false_type{}, std::true_type{});
-        arrive(X, ls);
-      };
-      const int hA = head_of(itA);
-      if (c_real && !c_pre && (s.presum || head_of(itC) == hA)) {
-        presum(itC, cb, c_dma);
-        c_pre = true;
-      }
-      if (itD >= 0 && !beyond(itD) && (s.presum || head_of(itD) == hA)) {
-        presum(itD, db, d_dma);
-        d_pre = true;
-      }
-      if (wave == 0) {
-        uint32_t spins = 0;
-        for (;;) {
-          uint64_t v[2][kFusedReps];
-          poll_issue(hA, v);
-          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-          st = poll_finish(v);
-          if (st != 0) break;
-          __builtin_amdgcn_s_sleep(2);
-          // Never expected: a wait past its limit (or after another group's
-          // did) flags the status word and gives up on the head.
-          ++spins;
-          if (spins > kFusedSpinLimit || ((spins & 255u) == 0u && (load_coherent(s.status) & 2u))) {
-            st = 2;
-            if (lane == 0) atomicOr(s.status, 2u);
-            break;
-          }
-        }
-        if (lane == 0) state_s = st;
-      }
-      __syncthreads();
-      st = state_s;
-    }
-    if (itA >= 0 && st == 1) pass2(itA, Ea);
-    if (q_dirty && c_real) load_q(head_of(itC), qf, rr);
-    if (wave != 0 || q_dirty) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    int nb = -1;
-    if (itC >= 0) {
-      if (!c_real) {
-        zero_item(itC);
-      } else {
-        float ls[2][4];
-        if (c_pre) {
-          pass1(cb, key0_of(itC), qf, rr, Ea, ls, std::true_type{}, std::false_type{});
-        } else {
-          pass1(cb, key0_of(itC), qf, rr, Ea, ls, std::true_type{}, std::true_type{});
-          arrive(itC, ls);
-        }
-        nb = itC;
-      }
-    }
-    // The next item's Q and R, loaded while this item is reduced.
-    const bool d_q = itD >= 0 && !beyond(itD);
-    if (d_q) load_q(head_of(itD), qf, rr);
-    itA = itB;
-    itB = nb;
-    itC = itD;
-    c_dma = d_dma;
-    c_pre = d_pre;
-    c_q = d_q;
-    d_dma = d_pre = false;
-    c_buf ^= 1;
-    return itA < 0 && itB < 0 && itC < 0;
-  };
-  for (;;) {
-    if (body(E0)) break;
-    if (body(E1)) break;
-  }
-  // Roles: body(Ea) reduces itA from Ea and refills Ea with itC; after the
-  // rotation the new itA is the old itB, whose E is the other buffer, hence the
-  // alternation.
-
-  // The last work-group to finish recomputes poisoned heads exactly.
-  wait_stores();
-  __syncthreads();
-  if (threadIdx.x == 0) last_s = atomicAdd(s.done, 1u) == gridDim.x - 1;
-  __syncthreads();
-  if (!last_s) return;
-  const int n_bad = (int)load_coherent(s.bad_n);
-  for (int ib = 0; ib < n_bad; ++ib) {
-    const int bh = (int)load_coherent(s.bad_list + ib);
-    const __amdgpu_buffer_rsrc_t rs = rsrc_of(bh);
-    const uint32_t voff = (uint32_t)r16 * row_bytes + 16u * (uint32_t)g;
-    load_q(bh, qf, rr);
-    float ref[2][4], wgt[2][4];
-    const int n_tiles_vis = a.p_last / 16 + 1;
-    // Sweep 0: the exact maximum of every row; sweep 1: its sum; sweep 2: F.
-    for (int sweep = 0; sweep < 2; ++sweep) {
-      float m[2][4];
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) m[pb][e] = sweep == 0 ? -INFINITY : 0.f;
-      for (int t = 0; t < n_tiles_vis; ++t) {
-        frag_t kf[kS];
-        M::load_k(rs, voff + (uint32_t)(16 * t) * row_bytes, kf);
-#pragma unroll
-        for (int pb = 0; pb < 2; ++pb) {
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < kS; ++ks) acc = M::mma(qf[pb][ks], kf[ks], acc);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool vis = 16 * t + r16 <= pos_s[w0 + 16 * pb + 4 * g + e];
-            if (sweep == 0) m[pb][e] = vis ? fmaxf(m[pb][e], acc[e]) : m[pb][e];
-            else m[pb][e] += vis ? fast_exp2(fmaf(acc[e], c2, -ref[pb][e])) : 0.f;
-          }
-        }
-      }
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (sweep == 0) ref[pb][e] = row_max16(m[pb][e]) * c2;
-          else wgt[pb][e] = 1.f / row_sum16(m[pb][e]);
-        }
-    }
-    float* F = s.scores + (int64_t)bh * a.L;
-    const int n_tiles = (a.L + 15) / 16;
-    for (int t = 0; t < n_tiles; ++t) {
-      float cs = 0.f;
-      if (t < n_tiles_vis) {
-        frag_t kf[kS];
-        M::load_k(rs, voff + (uint32_t)(16 * t) * row_bytes, kf);
-#pragma unroll
-        for (int pb = 0; pb < 2; ++pb) {
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int ks = 0; ks < kS; ++ks) acc = M::mma(qf[pb][ks], kf[ks], acc);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool vis = 16 * t + r16 <= pos_s[w0 + 16 * pb + 4 * g + e];
-            cs += vis ? fast_exp2(fmaf(acc[e], c2, -ref[pb][e])) * wgt[pb][e] : 0.f;
-          }
-        }
-      }
-      cs = sum_over_groups(cs);
-      __syncthreads();
-      if (g == 0) stage_s[wave][r16] = cs;
-      __syncthreads();
-      if (wave == 0 && lane < 16) {
-        const float f = ((stage_s[0][lane] + stage_s[1][lane]) + stage_s[2][lane]) + stage_s[3][lane];
-        if (16 * t + lane < a.L) F[16 * t + lane] = f;
-        fcol_s[lane] = f;
-      }
-      if (s.gkeys) {
-        __syncthreads();
-        const int j0 = 16 * t + 4 * (int)threadIdx.x;
-        if (threadIdx.x < 4 && j0 < a.L) {
-          const int n = min(4, a.L - j0);
-          float fv[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) fv[e] = fcol_s[4 * threadIdx.x + e];
-          uint32_t kv[4];
-          gumbel_block_keys(s.g_mode, j0, n, bh / a.H, bh % a.H, s.g_layer, s.g_k0, s.g_k1, fv, kv);
-          uint32_t* gk = s.gkeys + (int64_t)bh * a.L;
-          for (int e = 0; e < n; ++e) gk[j0 + e] = kv[e];
-        }
-      }
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
 // Host-side launchers.
 
 namespace {
@@ -1802,34 +1243,7 @@ hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
   return launch_score_split_t(score_split_kernel, L, stream);
 }
 
-int score_fused_resident() {
-  int per_cu = 0, dev = 0, cus = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_fused_kernel, kScoreThreads, 0) != hipSuccess)
-    return 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  return per_cu * cus;
-}
-
-hipError_t launch_score_fused(const ScoreLaunch& L, hipStream_t stream) {
-  // Every wait ends only if the resident work-groups outnumber half a head's
-  // chunks; the launch asks for at least a whole head's worth.
-  const int grid = std::min(L.sched.total_items, score_fused_resident());
-  if (grid < 1 || grid < L.sched.n_vis || !score_fused_shape(L.dtype, L.D, L.args.P) || L.sched.lse_given)
-    return hipErrorInvalidValue;
-  const int BH = L.args.B * L.args.H;
-  const __bf16* q = static_cast<const __bf16*>(L.q);
-  const __bf16* k = static_cast<const __bf16*>(L.k);
-  hipLaunchKernelGGL(score_fused_init_kernel, dim3(BH), dim3(kScoreThreads), 0, stream, q, k, L.args, L.sched,
-                     L.n_counter_words);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(score_fused_kernel, dim3(grid), dim3(kScoreThreads), 0, stream, q, k, L.args, L.sched);
-  return hipGetLastError();
-}
-
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream) {
-  if (L.sched.fused) return launch_score_fused(L, stream);
   if (score_uses_split(L.dtype, L.D, L.args.P)) {
     if (L.sched.chunk_keys != kSplitChunkKeys) return hipErrorInvalidValue;
     return launch_score_split(L, stream);

@@ -27,8 +27,8 @@ SAMPLE_SOFTMAX = 0
 SAMPLE_PROPORTIONAL = 1
 SAMPLE_UNIFORM = 2
 
-EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_evict",
-            "nacl_status_string", "nacl_last_error_detail", "nacl_version")
+EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_append",
+            "nacl_evict", "nacl_status_string", "nacl_last_error_detail", "nacl_version")
 
 
 class NaclError(RuntimeError):
@@ -71,6 +71,8 @@ def load_library(path=LIB_PATH):
     lib.nacl_select.restype = ctypes.c_int
     lib.nacl_compact.argtypes = [P, vp, vp, vp, i32, vp, vp, vp]
     lib.nacl_compact.restype = ctypes.c_int
+    lib.nacl_append.argtypes = [P, vp, vp, i32, vp, vp, i32, vp]
+    lib.nacl_append.restype = ctypes.c_int
     lib.nacl_evict.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, vp, sz, vp]
     lib.nacl_evict.restype = ctypes.c_int
     lib.nacl_status_string.argtypes = [ctypes.c_int]
@@ -191,11 +193,20 @@ def workspace_bytes(prob):
 
 
 def workspace(prob, device="cuda"):
+    """A workspace for prob, zeroed so that its sticky health word starts
+    clean (the library itself needs no initialised contents)."""
     n = workspace_bytes(prob)
     if n == 0:
         lib = load_library()
         raise NaclError(NACL_ERR_INVALID_ARG, lib.nacl_last_error_detail().decode())
-    return torch.empty(n, dtype=torch.uint8, device=device)
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def health(ws):
+    """(this call's, sticky) health words of a workspace (include/nacl.h);
+    reading them waits for the stream."""
+    w = ws[4:12].view(torch.int32).cpu()
+    return int(w[0]), int(w[1])
 
 
 def score(prob, q, k, ws, lse=None, out=None):
@@ -231,29 +242,48 @@ def select(prob, scores, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
     return out
 
 
-def compact(prob, k, v, keep_idx, k_out=None, v_out=None):
-    """K', V' [B, H, C, D] (Section 3)."""
+def compact(prob, k, v, keep_idx, k_out=None, v_out=None, in_place=False):
+    """K', V' [B, H, C, D] (Section 3).  in_place: the kept rows move to rows
+    0..C-1 of each head of k and v themselves (generation-phase cache)."""
     lib = load_library()
     dev = _gpu(k, "k", k.device).device
     prob.qkv(k, "k", dev, "k")
     prob.qkv(v, "v", dev, "v")
     C = keep_idx.shape[-1]
     _gpu(keep_idx, "keep_idx", dev, (prob.B, prob.H, C), torch.int32, contiguous=True)
-    if k_out is None:
-        k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=k.device)
-    if v_out is None:
-        v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=v.device)
-    for t, name in ((k_out, "k_out"), (v_out, "v_out")):
-        _gpu(t, name, dev, (prob.B, prob.H, C, prob.D), prob.torch_dtype, contiguous=True)
+    if in_place:
+        k_out, v_out = k, v
+    else:
+        if k_out is None:
+            k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=k.device)
+        if v_out is None:
+            v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=v.device)
+        for t, name in ((k_out, "k_out"), (v_out, "v_out")):
+            _gpu(t, name, dev, (prob.B, prob.H, C, prob.D), prob.torch_dtype, contiguous=True)
     _check(lib.nacl_compact(prob.ref(), _ptr(k), _ptr(v), _ptr(keep_idx), int(C), _ptr(k_out),
                             _ptr(v_out), _stream(k.device)))
     return k_out, v_out
 
 
+def append(prob, k, v, row0, k_new, v_new):
+    """Rows [row0, row0 + m) of every head of the cache k, v take k_new, v_new
+    [B, H, m, D] (Algorithm 1, generation phase)."""
+    lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    prob.qkv(k, "k", dev, "k")
+    prob.qkv(v, "v", dev, "v")
+    m = k_new.shape[2]
+    for t, name in ((k_new, "k_new"), (v_new, "v_new")):
+        _gpu(t, name, dev, (prob.B, prob.H, m, prob.D), prob.torch_dtype, contiguous=True)
+    _check(lib.nacl_append(prob.ref(), _ptr(k), _ptr(v), int(row0), _ptr(k_new), _ptr(v_new), int(m),
+                           _stream(k.device)))
+
+
 def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=None,
-          scores=None, keep_idx=None, k_out=None, v_out=None):
+          scores=None, keep_idx=None, k_out=None, v_out=None, in_place=False):
     """score -> select -> compact on the current stream.  Returns
-    (scores, keep_idx, k_out, v_out)."""
+    (scores, keep_idx, k_out, v_out); with in_place the kept rows move to rows
+    0..C-1 of each head of k and v, which are returned as k_out and v_out."""
     lib = load_library()
     dev = _gpu(k, "k", k.device).device
     for t, name in ((q, "q"), (k, "k"), (v, "v")):
@@ -264,15 +294,18 @@ def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
         scores = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=dev)
     if keep_idx is None:
         keep_idx = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=dev)
-    if k_out is None:
-        k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=dev)
-    if v_out is None:
-        v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=dev)
+    if in_place:
+        k_out, v_out = k, v
+    else:
+        if k_out is None:
+            k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=dev)
+        if v_out is None:
+            v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=dev)
+        for t, name in ((k_out, "k_out"), (v_out, "v_out")):
+            _gpu(t, name, dev, (prob.B, prob.H, int(C), prob.D), prob.torch_dtype, contiguous=True)
     _gpu(ws, "ws", dev, dtype=torch.uint8, contiguous=True)
     _gpu(scores, "scores", dev, (prob.B, prob.H, prob.L), torch.float32, contiguous=True)
     _gpu(keep_idx, "keep_idx", dev, (prob.B, prob.H, int(C)), torch.int32, contiguous=True)
-    for t, name in ((k_out, "k_out"), (v_out, "v_out")):
-        _gpu(t, name, dev, (prob.B, prob.H, int(C), prob.D), prob.torch_dtype, contiguous=True)
     _check(lib.nacl_evict(prob.ref(), _ptr(q), _ptr(k), _ptr(v), int(C), int(Cr), int(sampling),
                           int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(k_out),
                           _ptr(v_out), _ptr(ws), ws.numel(), _stream(dev)))

@@ -30,7 +30,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(nacl.EXPORTED)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.nacl_version() == 1
+    assert lib.nacl_version() == 2
 
 
 def _prob(**kw):
@@ -111,3 +111,42 @@ def test_status_strings(lib):
     for code in range(5):
         assert lib.nacl_status_string(code)
     assert lib.nacl_status_string(99) == b"unknown status"
+
+
+def test_in_place_compaction_checks(lib):
+    """In-place compaction needs k_out == k and v_out == v together, K and V in
+    disjoint memory, and keep_idx outside both; anything else is refused
+    before a launch."""
+    p = _prob()
+    k = 1 << 30
+    kbytes = 2 * 4 * 1000 * 128 * 2
+    K, V, KEEP = (ctypes.c_void_p(x) for x in (k, k + 2 * kbytes, k + 8 * kbytes))
+    # only k aliased
+    st = lib.nacl_compact(p.ref(), K, V, KEEP, 200, K, ctypes.c_void_p(k + 4 * kbytes), None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # K and V overlap
+    Vo = ctypes.c_void_p(k + 4096)
+    st = lib.nacl_compact(p.ref(), K, Vo, KEEP, 200, K, Vo, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # keep_idx inside K
+    st = lib.nacl_compact(p.ref(), K, V, ctypes.c_void_p(k + 1024), 200, K, V, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("row0,m", [(-1, 4), (990, 11), (0, -1)])
+def test_append_range_checks(lib, row0, m):
+    p = _prob()
+    k = 1 << 30
+    kbytes = 2 * 4 * 1000 * 128 * 2
+    st = lib.nacl_append(p.ref(), ctypes.c_void_p(k), ctypes.c_void_p(k + 2 * kbytes), row0,
+                         ctypes.c_void_p(k + 8 * kbytes), ctypes.c_void_p(k + 9 * kbytes), m, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG, lib.nacl_last_error_detail()
+
+
+def test_append_overlap_rejected(lib):
+    p = _prob()
+    k = 1 << 30
+    kbytes = 2 * 4 * 1000 * 128 * 2
+    st = lib.nacl_append(p.ref(), ctypes.c_void_p(k), ctypes.c_void_p(k + 2 * kbytes), 10,
+                         ctypes.c_void_p(k + 4096), ctypes.c_void_p(k + 9 * kbytes), 4, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG

@@ -88,20 +88,6 @@ def test_prefill_32k_layer(layer):
     _say(f"  {len(heads)} heads compared, {n} near-tie differences")
 
 
-def test_prefill_32k_single_read(monkeypatch):
-    """Layer 0 of the 32k workload through the opt-in single-read score kernel
-    (256 items of 128 keys per head on the resident work-groups): all heads'
-    properties, three heads against the oracle."""
-    monkeypatch.setenv("NACL_SCORE_PATH", "fused")
-    w = WORKLOADS["prefill_32k"]
-    _say("prefill_32k single-read")
-    q, k, v, F, keep, ko, vo = _evict(w, 0)
-    _properties(w, F, keep)
-    heads = [(0, 0), (2, 19), (3, 31)]
-    n = _check_heads(w, 0, q, k, v, F, keep, ko, vo, heads, "32k single-read")
-    _say(f"  {len(heads)} heads compared, {n} near-tie differences")
-
-
 def test_sweep_16k_all_budgets():
     """Batch 8 x 32 heads x 16384 tokens; budgets 10/20/50 % with random
     shares 0/25/50 %: scores once, then selection and compaction per budget."""

@@ -61,13 +61,12 @@ SCORE_CASES = [
     # 2048-key items with a ragged tail, and proxies early so later items lie past them
     ("bf16_split_scattered", 1, 2, 5001, 128, "bf16", sorted(set(range(7, 5001, 31)))),
     ("bf16_split_early", 2, 1, 4100, 128, "bf16", list(range(200, 330))),
-    # 128 proxies (the single-read kernel's shape, see test_score_single_read): 128-key
-    # items with a ragged tail, scattered proxies, items past the last proxy, proxies at
-    # the start
-    ("bf16_fused_suffix", 2, 3, 1000, 128, "bf16", list(range(872, 1000))),
-    ("bf16_fused_scattered", 1, 2, 5001, 128, "bf16", [7 + 39 * i for i in range(128)]),
-    ("bf16_fused_early", 2, 1, 4100, 128, "bf16", list(range(200, 328))),
-    ("bf16_fused_first", 1, 3, 300, 128, "bf16", list(range(128))),
+    # exactly 128 proxies (the benchmark's proxy count): a ragged tail, scattered
+    # proxies, items past the last proxy, proxies at the start
+    ("bf16_p128_suffix", 2, 3, 1000, 128, "bf16", list(range(872, 1000))),
+    ("bf16_p128_scattered", 1, 2, 5001, 128, "bf16", [7 + 39 * i for i in range(128)]),
+    ("bf16_p128_early", 2, 1, 4100, 128, "bf16", list(range(200, 328))),
+    ("bf16_p128_first", 1, 3, 300, 128, "bf16", list(range(128))),
     # more than 512 proxies: the wide proxy-split kernel over two and three groups of 512
     # (column sums accumulated across groups), and the per-wave-tile kernel for fp32
     ("bf16_wide_two_groups", 1, 2, 3000, 128, "bf16", sorted(set(range(5, 3000, 5)))),
@@ -124,17 +123,14 @@ def test_score_with_caller_lse(P):
 
 
 @pytest.mark.parametrize("P", [100, 128, 160, 600])
-def test_score_overflow_takes_exact_path(P, monkeypatch):
+def test_score_overflow_takes_exact_path(P):
     """Pass 1 sums exp2(logit - r) against the maximum r of the first tile of
     each item's key range; a later key far above r overflows fp32, and the
     kernel recomputes that range's sums against its exact maximum.  Here one
     key per head sits about 180 (natural-log units) above every other logit
     of its range, so the fast path overflows and the scores are dominated by
-    that key (P = 160: the proxy-split kernel; P = 600: its wide form; P = 128:
-    the single-read kernel, whose row sums leave their fixed-point range, so both
-    heads are recomputed by its exact path)."""
-    if P == 128:
-        monkeypatch.setenv("NACL_SCORE_PATH", "fused")
+    that key (P = 100: the per-wave-tile kernel; P = 128 and 160: the
+    proxy-split kernel; P = 600: its wide form)."""
     B, H, L, D = 1, 2, 3000, 128
     g = torch.Generator(device="cuda").manual_seed(11)
     q = torch.randn((B, H, L, D), generator=g, device="cuda")
@@ -151,43 +147,6 @@ def test_score_overflow_takes_exact_path(P, monkeypatch):
     check_scores(F.cpu().numpy(), Fr, "overflow")
     for h, j in ((0, 1000), (1, 2500)):  # nearly all the mass of every proxy that sees key j
         assert float(F[0, h, j]) > 0.99 * sum(p >= j for p in pos)
-
-
-FUSED_CASES = [c for c in SCORE_CASES if c[0].startswith("bf16_fused")]
-
-
-@pytest.mark.parametrize("path", ["fused", "presum"])
-@pytest.mark.parametrize("case", FUSED_CASES, ids=[c[0] for c in FUSED_CASES])
-def test_score_single_read(case, path, monkeypatch):
-    """The 128-proxy shapes through the single-read kernel (opt-in), as scheduled and
-    with every item summed ahead of its turn (its rarely taken progress path)."""
-    monkeypatch.setenv("NACL_SCORE_PATH", "fused")
-    if path == "presum":
-        monkeypatch.setenv("NACL_FUSED_PRESUM", "1")
-    name, B, H, L, D, dt, pos = case
-    _say("score case", name, path)
-    w = custom(name, B, H, L, D, len(pos), dtype=dt, data_seed=zlib.crc32(name.encode()) % 1000)
-    q, k, v = make_layer(w, 0, device="cuda")
-    prob = nacl.Problem.from_tensors(q, k, v, pos)
-    F = nacl.score(prob, q, k, nacl.workspace(prob))
-    torch.cuda.synchronize()
-    Fr, _ = proxy_scores(_np(q), _np(k), pos, prob.c.sm_scale)
-    check_scores(F.cpu().numpy(), Fr, f"{name}/{path}")
-
-
-def test_score_single_read_is_bit_reproducible(monkeypatch):
-    """The single-read kernel adds its row sums as integers, so the scores do not
-    depend on the order in which a head's items arrive."""
-    monkeypatch.setenv("NACL_SCORE_PATH", "fused")
-    name, B, H, L, D, dt, pos = FUSED_CASES[1]
-    w = custom(name, B, H, L, D, len(pos), dtype=dt, data_seed=5)
-    q, k, v = make_layer(w, 0, device="cuda")
-    prob = nacl.Problem.from_tensors(q, k, v, pos)
-    ws = nacl.workspace(prob)
-    F1 = nacl.score(prob, q, k, ws).clone()
-    F2 = nacl.score(prob, q, k, ws)
-    torch.cuda.synchronize()
-    assert torch.equal(F1.view(torch.int32), F2.view(torch.int32))
 
 
 def test_score_config_small_and_longbench():
@@ -354,16 +313,15 @@ def test_evict_is_deterministic():
 @pytest.mark.parametrize("mode", [SAMPLE_SOFTMAX, SAMPLE_PROPORTIONAL, SAMPLE_UNIFORM])
 @pytest.mark.parametrize("where", ["end", "early"])
 @pytest.mark.parametrize("P", [40, 128, 160])
-def test_evict_draws_the_same_keys_as_select(mode, where, P, monkeypatch):
+def test_evict_draws_the_same_keys_as_select(mode, where, P):
     """nacl_evict draws the Gumbel keys inside the column reduction (skipping
     the selection's key kernel); its keep set must equal that of nacl_select
     run on the same scores, which draws every key in its own kernel.  Proxies
     at the end, or early so that whole chunks lie past the last proxy (scores
     0, keys drawn on the zero path); L not a multiple of 4; every non-protected
     slot random, so every key's value matters.  P = 160 runs the proxy-split
-    score kernel, P = 128 the single-read one, P = 40 the per-wave-tile one."""
-    if P == 128:
-        monkeypatch.setenv("NACL_SCORE_PATH", "fused")
+    score kernel on one proxy group (P = 128) and on a full and a partial group
+    (P = 160), P = 40 the per-wave-tile one."""
     B, H, L, D = 2, 3, 9001, 128
     pos = list(range(L - P, L)) if where == "end" else list(range(300, 300 + P))
     _say("evict keys", mode, where, P)
