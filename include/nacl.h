@@ -166,6 +166,25 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
                float* scores, int32_t* keep_idx, void* k_out, void* v_out,
                void* ws, size_t ws_bytes, void* stream);
 
+/* The whole step without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  Arguments and results as nacl_evict,
+ * which it runs; p->proxy_pos_dev is required (no host-to-device copy).  The
+ * workspace is a built-in device array of NACL_NOALLOC_WORKSPACE_MAX bytes,
+ * one per GPU, held until the process ends; problems needing more
+ * (nacl_workspace_bytes) return NACL_ERR_UNSUPPORTED.  Nothing is allocated:
+ * no hipMalloc, hipFree or allocating library routine.  Every call on a GPU
+ * shares that GPU's array, so calls on one GPU that overlap in time (other
+ * streams, other threads) race and must be serialised by the caller.
+ * health: optional device uint32[2] that receives the call's health words
+ * (this call's, then the sticky one accumulated over every such call on the
+ * GPU; see nacl_score), copied on the stream after the eviction. */
+#define NACL_NOALLOC_WORKSPACE_MAX (64u << 20)
+int nacl_evict_noalloc(const nacl_problem* p, const void* q, const void* k, const void* v,
+                       int32_t C, int32_t Cr, int32_t sampling, uint64_t seed, uint32_t layer,
+                       float* scores, int32_t* keep_idx, void* k_out, void* v_out,
+                       uint32_t* health, void* stream);
+
 /* Static text for a status code. */
 const char* nacl_status_string(int status);
 

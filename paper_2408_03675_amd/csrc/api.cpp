@@ -26,6 +26,18 @@ int fail(int status, const char* fmt, ...) {
   return status;
 }
 
+}  // namespace
+
+int nacl::fail_status(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_detail, sizeof(g_detail), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+namespace {
+
 int hip_fail(hipError_t e, const char* what) {
   return fail(NACL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }

@@ -8,6 +8,9 @@
 
 namespace nacl {
 
+// Sets the thread-local error text of the C ABI and returns status.
+int fail_status(int status, const char* fmt, ...);
+
 // Score kernel shape.  A work item spans kScoreWaves waves x tpw tiles of 16
 // keys; kScoreWavesPerSimd is the occupancy the register allocation targets.
 #ifndef NACL_SCORE_TPW_MAX

@@ -28,7 +28,8 @@ SAMPLE_PROPORTIONAL = 1
 SAMPLE_UNIFORM = 2
 
 EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_append",
-            "nacl_evict", "nacl_status_string", "nacl_last_error_detail", "nacl_version")
+            "nacl_evict", "nacl_evict_noalloc", "nacl_status_string", "nacl_last_error_detail",
+            "nacl_version")
 
 
 class NaclError(RuntimeError):
@@ -75,6 +76,8 @@ def load_library(path=LIB_PATH):
     lib.nacl_append.restype = ctypes.c_int
     lib.nacl_evict.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, vp, sz, vp]
     lib.nacl_evict.restype = ctypes.c_int
+    lib.nacl_evict_noalloc.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, vp, vp]
+    lib.nacl_evict_noalloc.restype = ctypes.c_int
     lib.nacl_status_string.argtypes = [ctypes.c_int]
     lib.nacl_status_string.restype = ctypes.c_char_p
     lib.nacl_last_error_detail.argtypes = []
@@ -309,4 +312,40 @@ def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
     _check(lib.nacl_evict(prob.ref(), _ptr(q), _ptr(k), _ptr(v), int(C), int(Cr), int(sampling),
                           int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(k_out),
                           _ptr(v_out), _ptr(ws), ws.numel(), _stream(dev)))
+    return scores, keep_idx, k_out, v_out
+
+
+NOALLOC_WORKSPACE_MAX = 64 << 20
+
+
+def evict_noalloc(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0,
+                  scores=None, keep_idx=None, k_out=None, v_out=None, health=None):
+    """nacl_evict_noalloc: the same step with the library's built-in device
+    scratch as workspace (no workspace argument).  prob must carry a device
+    copy of the proxy positions.  health: optional int32 [2] GPU tensor that
+    receives the call's health words.  Outputs must be given or are
+    allocated here by torch before the call (the library allocates
+    nothing)."""
+    lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        prob.qkv(t, name, dev, name)
+    if scores is None:
+        scores = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=dev)
+    if keep_idx is None:
+        keep_idx = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=dev)
+    if k_out is None:
+        k_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=k.dtype, device=dev)
+    if v_out is None:
+        v_out = torch.empty((prob.B, prob.H, C, prob.D), dtype=v.dtype, device=dev)
+    _gpu(scores, "scores", dev, (prob.B, prob.H, prob.L), torch.float32, contiguous=True)
+    _gpu(keep_idx, "keep_idx", dev, (prob.B, prob.H, int(C)), torch.int32, contiguous=True)
+    if k_out is not k:
+        for t, name in ((k_out, "k_out"), (v_out, "v_out")):
+            _gpu(t, name, dev, (prob.B, prob.H, int(C), prob.D), prob.torch_dtype, contiguous=True)
+    if health is not None:
+        _gpu(health, "health", dev, (2,), torch.int32, contiguous=True)
+    _check(lib.nacl_evict_noalloc(prob.ref(), _ptr(q), _ptr(k), _ptr(v), int(C), int(Cr), int(sampling),
+                                  int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(k_out),
+                                  _ptr(v_out), _ptr(health), _stream(dev)))
     return scores, keep_idx, k_out, v_out
