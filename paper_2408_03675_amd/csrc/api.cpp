@@ -48,8 +48,10 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
 
 struct Layout {
-  size_t cnt, pos, lse, part, keys, total;
+  size_t cnt, pos, lse, part, keys, samples, rounds, mid, total;
   int n_chunks;
+  size_t sel_sync_word;   // first word of the selection's sync region inside the counter section
+  int n_counter_words;    // counter words cleared before the score kernel (all but the sticky word)
 };
 
 constexpr int kCounterHeader = 64;  // queue + status words, padded to 256 bytes
@@ -60,7 +62,11 @@ Layout layout_of(const nacl_problem* p) {
   l.n_chunks = (p->L + nacl::kScoreMinChunkKeys - 1) / nacl::kScoreMinChunkKeys;  // most chunks any call uses
   size_t off = 0;
   l.cnt = off;
-  off += align_up((kCounterHeader + BH) * sizeof(uint32_t));  // header, per-head counters
+  // header, the score's per-head counters, then the selection's ticket
+  // (padded to 64 words) and per-head round counters
+  l.sel_sync_word = kCounterHeader + BH;
+  l.n_counter_words = (int)(kCounterHeader + BH + 64 + BH);
+  off += align_up((size_t)l.n_counter_words * sizeof(uint32_t));
   l.pos = off;
   off += align_up((size_t)p->P * sizeof(int32_t));
   l.lse = off;
@@ -69,6 +75,16 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up(BH * l.n_chunks * p->P * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
+  // The sliced selection of long heads exchanges samples, counts and
+  // candidate lists through these.
+  const bool sliced = nacl::select_uses_slices(p->L);
+  const size_t nb = nacl::select_slices(p->L);
+  l.samples = off;
+  if (sliced) off += align_up(BH * 2 * nacl::select_sample_slots(p->L) * sizeof(uint32_t));
+  l.rounds = off;
+  if (sliced) off += align_up(BH * 2 * nb * 2 * sizeof(uint32_t));
+  l.mid = off;
+  if (sliced) off += align_up(BH * 2 * nb * nacl::select_cap_block(p->L) * 2 * sizeof(uint32_t));
   l.total = off;
   return l;
 }
@@ -216,7 +232,7 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   sc.g_k0 = (uint32_t)(kd.seed & 0xFFFFFFFFu);
   sc.g_k1 = (uint32_t)(kd.seed >> 32);
   sc.g_layer = kd.layer;
-  s.n_counter_words = kCounterHeader + BH;
+  s.n_counter_words = l.n_counter_words;
   // Item size: the largest tpw whose items still number at least four per
   // resident work-group (two per CU); long items amortise the per-item Q
   // loads, partial stores and pipeline fill, too few leave a long tail.
@@ -248,7 +264,7 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
 
 int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr, int32_t sampling,
                uint64_t seed, uint32_t layer, int32_t* keep, char* ws, const Layout& l,
-               const int* pos_dev, hipStream_t stream, bool keys_ready = false) {
+               const int* pos_dev, hipStream_t stream, bool keys_ready = false, bool sync_zeroed = false) {
   if (C == 0) return NACL_OK;
   nacl::SelectLaunch s{};
   s.B = p->B;
@@ -267,6 +283,16 @@ int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr
   s.keys2 = reinterpret_cast<uint32_t*>(ws + l.keys);
   s.keep = keep;
   s.keys_ready = keys_ready ? 1 : 0;
+  s.nb = nacl::select_slices(p->L);
+  s.ms = nacl::select_sample_slots(p->L);
+  s.cap_b = nacl::select_cap_block(p->L);
+  uint32_t* words = reinterpret_cast<uint32_t*>(ws + l.cnt);
+  s.sync = words + l.sel_sync_word;
+  s.samples = reinterpret_cast<uint32_t*>(ws + l.samples);
+  s.rounds = reinterpret_cast<uint32_t*>(ws + l.rounds);
+  s.mid = reinterpret_cast<uint32_t*>(ws + l.mid);
+  s.health = words + 1;
+  s.zero_sync = !sync_zeroed;
   hipError_t e = nacl::launch_select(s, stream);
   if (e != hipSuccess) return hip_fail(e, "select kernels");
   return NACL_OK;
@@ -452,7 +478,8 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
   kd.seed = seed;
   kd.layer = layer;
   if ((st = run_score(p, q, k, nullptr, scores, w, l, pos_dev, s, kd))) return st;
-  if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s, kd.on))) return st;
+  // The score kernel's counter clearing also cleared the selection's.
+  if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s, kd.on, true))) return st;
   uint32_t* health = reinterpret_cast<uint32_t*>(w + l.cnt) + 1;
   return run_compact(p, k, v, keep_idx, C, k_out, v_out, in_place, health, s);
 }
