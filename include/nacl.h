@@ -84,6 +84,15 @@ typedef struct nacl_problem {
   const int32_t* proxy_pos_dev; /* optional DEVICE copy of proxy_pos (same values);
                                 NULL: the library stages proxy_pos through the
                                 workspace with a stream-ordered copy */
+  int32_t q_group;           /* query heads per K/V head (grouped-query attention;
+                                0 or 1: multi-head, 1..64).  H counts K/V heads:
+                                K, V, scores, keep_idx and the outputs have H
+                                heads, Q has H * q_group heads (q_stride[1] steps
+                                one query head), and K/V head h is scored by the
+                                proxy rows of query heads h*q_group ..
+                                h*q_group + q_group - 1, so its score mass is
+                                P * q_group.  lse (nacl_score) is then
+                                [B, H * q_group, P]. */
 } nacl_problem;
 
 /* Workspace bytes the score, select and evict calls need for problem *p

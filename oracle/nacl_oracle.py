@@ -77,6 +77,37 @@ def proxy_scores(Q, K, proxy_pos, sm_scale):
     return F, lse
 
 
+def proxy_scores_grouped(Q, K, proxy_pos, sm_scale, q_group):
+    """F_score (Section 5.1) when several query heads share one K/V head
+    (grouped-query attention; the paper's LLaMA2-7B has one query head per
+    K/V head, so this is a reading for models that group them).
+
+    Reading: the attention rows that look at K/V head h are those of its
+    q_group query heads h * q_group .. h * q_group + q_group - 1, so K/V head h
+    is scored by the proxy rows of all of them: F[b, h] is the sum over the
+    group of each query head's F_score against the shared keys, and its score
+    mass is P * q_group.
+
+    Q: [B, H * q_group, L, D]; K: [B, H, L, D].  Returns (F [B, H, L],
+    lse [B, H * q_group, P]), float64.
+    """
+    Q = np.asarray(Q)
+    K = np.asarray(K)
+    B, H, L, D = K.shape
+    g = int(q_group)
+    if Q.shape[1] != H * g:
+        raise ValueError("Q must have H * q_group heads")
+    F = np.zeros((B, H, L), dtype=np.float64)
+    lse = np.zeros((B, H * g, len(proxy_pos)), dtype=np.float64)
+    for h in range(H):
+        for e in range(g):
+            hq = h * g + e
+            Fe, le = proxy_scores(Q[:, hq:hq + 1], K[:, h:h + 1], proxy_pos, sm_scale)
+            F[:, h] += Fe[:, 0]
+            lse[:, hq] = le[:, 0]
+    return F, lse
+
+
 def protected_set(proxy_pos, n_protect):
     """Pi: the proxy tokens kept by default (Section 5.1: proxies are retained).
 

@@ -47,6 +47,10 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
 
+// Query heads per K/V head (0 means 1), and proxy rows per K/V head.
+int q_group_of(const nacl_problem* p) { return p->q_group > 1 ? p->q_group : 1; }
+int rows_of(const nacl_problem* p) { return p->P * q_group_of(p); }
+
 struct Layout {
   size_t cnt, pos, lse, part, keys, samples, rounds, mid, total;
   int n_chunks;
@@ -69,10 +73,11 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up((size_t)l.n_counter_words * sizeof(uint32_t));
   l.pos = off;
   off += align_up((size_t)p->P * sizeof(int32_t));
+  const size_t rows = (size_t)rows_of(p);
   l.lse = off;
-  off += align_up(BH * p->P * sizeof(float));
+  off += align_up(BH * rows * sizeof(float));
   l.part = off;
-  off += align_up(BH * l.n_chunks * p->P * sizeof(float2));
+  off += align_up(BH * l.n_chunks * rows * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
   // The sliced selection of long heads exchanges samples, counts and
@@ -112,6 +117,10 @@ int check_problem(const nacl_problem* p) {
     return fail(NACL_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
   if (p->P < 1 || p->P > p->L) return fail(NACL_ERR_INVALID_ARG, "P must lie in [1, L] (got %d)", p->P);
   if (p->P > NACL_MAX_P) return fail(NACL_ERR_UNSUPPORTED, "P = %d exceeds %d", p->P, NACL_MAX_P);
+  if (p->q_group < 0 || p->q_group > 64)
+    return fail(NACL_ERR_INVALID_ARG, "q_group must lie in [0, 64] (got %d)", p->q_group);
+  if ((int64_t)p->B * p->H * q_group_of(p) > 65535)
+    return fail(NACL_ERR_UNSUPPORTED, "B * H * q_group exceeds 65535");
   if (p->n_protect < 0 || p->n_protect > p->P)
     return fail(NACL_ERR_INVALID_ARG, "n_protect must lie in [0, P] (got %d)", p->n_protect);
   if (!(std::isfinite(p->sm_scale) && p->sm_scale > 0.f))
@@ -203,7 +212,9 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   s.args.B = p->B;
   s.args.H = p->H;
   s.args.L = p->L;
-  s.args.P = p->P;
+  s.args.P = rows_of(p);  // proxy rows per K/V head
+  s.args.P0 = p->P;
+  s.args.qg = q_group_of(p);
   for (int i = 0; i < 3; ++i) {
     s.args.qs[i] = p->q_stride[i];
     s.args.ks[i] = p->k_stride[i];
@@ -245,9 +256,9 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   }
   sc.chunk_keys = sc.tpw * nacl::kScoreWaves * 16;
   // The proxy-split kernel takes fixed items of kSplitChunkKeys keys.
-  if (nacl::score_uses_split(p->dtype, p->D, p->P)) sc.chunk_keys = nacl::kSplitChunkKeys;
+  if (nacl::score_uses_split(p->dtype, p->D, rows_of(p))) sc.chunk_keys = nacl::kSplitChunkKeys;
   sc.n_chunks = (p->L + sc.chunk_keys - 1) / sc.chunk_keys;  // <= l.n_chunks
-  const int group_items = nacl::score_uses_split(p->dtype, p->D, p->P) ? NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
+  const int group_items = nacl::score_uses_split(p->dtype, p->D, rows_of(p)) ? NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
                                                                        : NACL_SCORE_GROUP_ITEMS_PER_CU;
   sc.heads_per_group = heads_per_group(BH, sc.n_chunks, group_items * cus);
   sc.n_groups = BH / sc.heads_per_group;

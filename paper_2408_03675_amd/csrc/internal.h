@@ -51,7 +51,8 @@ inline bool score_uses_split(int dtype, int D, int P) { return NACL_SCORE_SPLIT 
 constexpr int kScoreMinChunkKeys = std::min(kScoreTpwMin * kScoreWaves * 16, kSplitChunkKeys);
 
 struct ScoreArgs {
-  int B, H, L, P;
+  int B, H, L, P;   // P: proxy rows per K/V head = P0 * qg, row r = proxy r / qg of query head r % qg
+  int P0, qg;       // proxies, query heads per K/V head
   int64_t qs[3], ks[3];
   const int* pos;   // device, P entries
   int p_last;       // pos[P - 1]

@@ -265,6 +265,25 @@ __device__ __forceinline__ ItemRef decode_item(const ScoreSched& s, int i) {
   return ItemRef{kind, group * s.heads_per_group + r / s.n_chunks, r % s.n_chunks};
 }
 
+// Proxy row r of a K/V head is proxy r / qg of query head r % qg of its
+// group (rows sorted by position, so positions never decrease along the
+// rows).  Returns the row's position and sets qrow to the element offset of
+// its query from the group's first query head.
+__device__ __forceinline__ int row_position(const ScoreArgs& a, int r, int64_t& qrow) {
+  const int ip = r / a.qg, e = r - ip * a.qg;
+  const int p = a.pos[ip];
+  qrow = (int64_t)e * a.qs[1] + (int64_t)p * a.qs[2];
+  return p;
+}
+
+// Index of row r's log-sum-exp: the library's own [B*H, P] rows, or the
+// caller's [B, H * qg, P] per query head.
+__device__ __forceinline__ int64_t lse_index(const ScoreArgs& a, const ScoreSched& s, int bh, int r) {
+  if (!s.lse_given) return (int64_t)bh * a.P + r;
+  const int ip = r / a.qg, e = r - ip * a.qg;
+  return ((int64_t)bh * a.qg + e) * a.P0 + ip;
+}
+
 // Logits of one 16-key tile for proxy blocks [P0, P0 + N) into acc[0 .. N):
 // pass-1 orientation (rows = keys) when KROWS, pass-2 orientation (rows =
 // proxies) otherwise.
@@ -328,6 +347,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
   static_assert(kUnroll % KStage<T, D>::kDepth == 0 && kScoreTpwMin % kUnroll == 0, "tiles per wave vs ring");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kGroup];
+  __shared__ int64_t qrow_g[kGroup];  // element offset of each row's query from qb
   __shared__ float2 red[kScoreWaves][kGroup];
   __shared__ float2 mrg[kScoreThreads];
   __shared__ float col_lds[kScoreWaves][kMaxKeysPerWave];
@@ -360,7 +380,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     if (item >= s.total_items) break;
     const ItemRef it = decode_item(s, item);
     const int bh = it.bh, b = bh / a.H, h = bh % a.H;
-    const T* qb = q + b * a.qs[0] + h * a.qs[1];
+    const T* qb = q + b * a.qs[0] + (int64_t)h * a.qg * a.qs[1];  // first query head of the group
     const T* kb = k + b * a.ks[0] + h * a.ks[1];
     const int TPW = s.tpw;  // multiple of kUnroll, at most TPWMAX
     const int chunk_key0 = it.chunk * s.chunk_keys;
@@ -441,7 +461,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
     // Positions of the proxy group [g0, g0 + gn), -1 past its end.
     auto load_group = [&](int g0, int gn) {
       __syncthreads();
-      for (int i = threadIdx.x; i < kGroup; i += kScoreThreads) pos_g[i] = i < gn ? a.pos[g0 + i] : -1;
+      for (int i = threadIdx.x; i < kGroup; i += kScoreThreads) pos_g[i] = i < gn ? row_position(a, g0 + i, qrow_g[i]) : -1;
       __syncthreads();
     };
     // The Q fragments of the whole group (zeros past its end).
@@ -449,7 +469,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
         const int i = 16 * pb + r16;
-        if (i < gn) M::load(qb + (int64_t)pos_g[i] * a.qs[2], g, qf[pb]);
+        if (i < gn) M::load(qb + qrow_g[i], g, qf[pb]);
         else M::zero(qf[pb]);
       }
     };
@@ -655,7 +675,7 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         frag_t qf[PB][kS];
         load_q(gn, qf);
         for (int i = threadIdx.x; i < kGroup; i += kScoreThreads)
-          lse_g[i] = i < gn ? load_coherent(lse + (int64_t)bh * a.P + g0 + i) * lse_mul : INFINITY;
+          lse_g[i] = i < gn ? load_coherent(lse + lse_index(a, s, bh, g0 + i)) * lse_mul : INFINITY;
         __syncthreads();
         // This lane's partial column sums of the last four tiles; every
         // fourth tile they are reduced across lane groups and lane group g
@@ -786,6 +806,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
   static_assert(KS::kInstr == kScoreWaves, "one DMA instruction per wave and tile");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kSplitGroup];
+  __shared__ int64_t qrow_g[kSplitGroup];  // element offset of each row's query from qb
   __shared__ float2 mrg[kScoreThreads];
   __shared__ float col_lds[kSplitChunkKeys];
   __shared__ float stage[kScoreWaves][64];
@@ -816,7 +837,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
     if (item >= s.total_items) break;
     const ItemRef it = decode_item(s, item);
     const int bh = it.bh, b = bh / a.H, h = bh % a.H;
-    const T* qb = q + b * a.qs[0] + h * a.qs[1];
+    const T* qb = q + b * a.qs[0] + (int64_t)h * a.qg * a.qs[1];  // first query head of the group
     const T* kb = k + b * a.ks[0] + h * a.ks[1];
     const int chunk_key0 = it.chunk * kSplitChunkKeys;
     const bool beyond = chunk_key0 > a.p_last;
@@ -866,7 +887,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
     };
     auto load_group = [&](int g0, int gn) {
       __syncthreads();
-      for (int i = threadIdx.x; i < kSplitGroup; i += kScoreThreads) pos_g[i] = i < gn ? a.pos[g0 + i] : -1;
+      for (int i = threadIdx.x; i < kSplitGroup; i += kScoreThreads) pos_g[i] = i < gn ? row_position(a, g0 + i, qrow_g[i]) : -1;
       __syncthreads();
     };
     // This wave's Q fragments (zeros past the group's end) and the positions
@@ -875,7 +896,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
 #pragma unroll
       for (int pb = 0; pb < WB; ++pb) {
         const int i = w0 + 16 * pb + r16;
-        if (i < gn) M::load(qb + (int64_t)pos_g[i] * a.qs[2], g, qf[pb]);
+        if (i < gn) M::load(qb + qrow_g[i], g, qf[pb]);
         else M::zero(qf[pb]);
       }
       const int wn = min(max(gn - w0, 0), 16 * WB);
@@ -1086,7 +1107,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
         int first, last;
         load_wave_q(gn, qf, first, last);
         for (int i = threadIdx.x; i < kSplitGroup; i += kScoreThreads)
-          lse_g[i] = i < gn ? load_coherent(lse + (int64_t)bh * a.P + g0 + i) * lse_mul : INFINITY;
+          lse_g[i] = i < gn ? load_coherent(lse + lse_index(a, s, bh, g0 + i)) * lse_mul : INFINITY;
         __syncthreads();
         // With groups of 128 proxies this lane's eight log-sum-exps (rows
         // 4 g + e of its two proxy blocks) stay in registers for the whole

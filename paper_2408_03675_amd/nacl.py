@@ -48,6 +48,7 @@ class _Problem(ctypes.Structure):
         ("v_stride", ctypes.c_int64 * 3),
         ("proxy_pos", ctypes.POINTER(ctypes.c_int32)),
         ("proxy_pos_dev", ctypes.c_void_p),
+        ("q_group", ctypes.c_int32),
     ]
 
 
@@ -132,18 +133,20 @@ class Problem:
     alive.  `dtype` is "bf16" or "f32"."""
 
     def __init__(self, B, H, L, D, dtype, proxy_pos, n_protect=None, sm_scale=None,
-                 q_stride=None, k_stride=None, v_stride=None, proxy_pos_dev=None):
+                 q_stride=None, k_stride=None, v_stride=None, proxy_pos_dev=None, q_group=1):
         pos = [int(x) for x in proxy_pos]
         self._pos = (ctypes.c_int32 * max(1, len(pos)))(*pos)
         self.proxy_pos = pos
+        self.q_group = int(q_group)
         dense = (H * L * D, L * D, D)
+        dense_q = (H * self.q_group * L * D, L * D, D)
         s = _Problem()
         s.B, s.H, s.L, s.D = B, H, L, D
         s.dtype = NACL_F32 if dtype in ("f32", torch.float32) else NACL_BF16
         s.P = len(pos)
         s.n_protect = len(pos) if n_protect is None else int(n_protect)
         s.sm_scale = float(sm_scale) if sm_scale else 1.0 / (D ** 0.5)
-        s.q_stride[:] = q_stride or dense
+        s.q_stride[:] = q_stride or dense_q
         s.k_stride[:] = k_stride or dense
         s.v_stride[:] = v_stride or dense
         s.proxy_pos = ctypes.cast(self._pos, ctypes.POINTER(ctypes.c_int32))
@@ -154,13 +157,17 @@ class Problem:
                 raise ValueError("proxy_pos_dev must be a contiguous int32 GPU tensor with one entry per proxy")
         self._pos_dev = proxy_pos_dev
         s.proxy_pos_dev = None if proxy_pos_dev is None else proxy_pos_dev.data_ptr()
+        s.q_group = self.q_group
         self.c = s
 
     @classmethod
     def from_tensors(cls, q, k, v, proxy_pos, n_protect=None, sm_scale=None, proxy_pos_dev=None):
+        """q may have a multiple of k's heads (grouped-query attention)."""
         B, H, L, D = k.shape
+        if q.dim() != 4 or q.shape[1] % H:
+            raise ValueError("q must be [B, H * q_group, L, D] for k of [B, H, L, D]")
         return cls(B, H, L, D, k.dtype, proxy_pos, n_protect, sm_scale,
-                   _strides(q), _strides(k), _strides(v), proxy_pos_dev)
+                   _strides(q), _strides(k), _strides(v), proxy_pos_dev, q_group=q.shape[1] // H)
 
     @property
     def B(self):
@@ -188,7 +195,8 @@ class Problem:
     # Shapes the entry points expect.
     def qkv(self, t, name, dev, which):
         st = {"q": self.c.q_stride, "k": self.c.k_stride, "v": self.c.v_stride}[which]
-        return _gpu(t, name, dev, (self.B, self.H, self.L, self.D), self.torch_dtype, tuple(st))
+        heads = self.H * self.q_group if which == "q" else self.H
+        return _gpu(t, name, dev, (self.B, heads, self.L, self.D), self.torch_dtype, tuple(st))
 
 
 def workspace_bytes(prob):
@@ -220,7 +228,7 @@ def score(prob, q, k, ws, lse=None, out=None):
     prob.qkv(q, "q", dev, "q")
     prob.qkv(k, "k", dev, "k")
     if lse is not None:
-        _gpu(lse, "lse", dev, (prob.B, prob.H, prob.c.P), torch.float32, contiguous=True)
+        _gpu(lse, "lse", dev, (prob.B, prob.H * prob.q_group, prob.c.P), torch.float32, contiguous=True)
     _gpu(ws, "ws", dev, dtype=torch.uint8, contiguous=True)
     if out is None:
         out = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=k.device)

@@ -2,5 +2,5 @@
 
 from .workloads import (  # noqa: F401
     Workload, WORKLOADS, SWEEP_KEEP, SWEEP_RANDOM, PAPER_RANDOM_SHARE_20,
-    sweep_workloads, custom, make_layer, alg_bytes, alg_flops,
+    sweep_workloads, custom, make_layer, make_grouped_layer, alg_bytes, alg_flops,
 )

@@ -163,6 +163,20 @@ def make_layer(w, layer=0, device="cpu"):
     return q.to(dt), k.to(dt), v.to(dt)
 
 
+def make_grouped_layer(w, q_group, layer=0, device="cpu"):
+    """Q [B, H * q_group, L, D] and K, V [B, H, L, D] for grouped-query
+    attention (several query heads per K/V head): N(0, 1) drawn in fp32 from
+    a torch.Generator seeded with data_seed + 1000 * layer (Q first, then K,
+    then V), rounded to w.dtype; no injection."""
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(w.data_seed) + 1000 * int(layer))
+    q = torch.randn((w.B, w.H * q_group, w.L, w.D), generator=gen, device=device, dtype=torch.float32)
+    k = torch.randn((w.B, w.H, w.L, w.D), generator=gen, device=device, dtype=torch.float32)
+    v = torch.randn((w.B, w.H, w.L, w.D), generator=gen, device=device, dtype=torch.float32)
+    dt = w.torch_dtype()
+    return q.to(dt), k.to(dt), v.to(dt)
+
+
 def alg_bytes(w):
     """Algorithmic HBM bytes of one layer, per stage (inputs read once,
     outputs written once).  Used for roofline fractions."""

@@ -150,3 +150,17 @@ def test_append_overlap_rejected(lib):
     st = lib.nacl_append(p.ref(), ctypes.c_void_p(k), ctypes.c_void_p(k + 2 * kbytes), 10,
                          ctypes.c_void_p(k + 4096), ctypes.c_void_p(k + 9 * kbytes), 4, None)
     assert st == nacl.NACL_ERR_INVALID_ARG
+
+
+def test_q_group_validation(lib):
+    p = _prob()
+    p.c.q_group = 65
+    st = lib.nacl_score(p.ref(), FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    p.c.q_group = -1
+    assert lib.nacl_score(p.ref(), FAKE, FAKE, None, FAKE, FAKE, 1 << 30, None) == nacl.NACL_ERR_INVALID_ARG
+    # the workspace holds one log-sum-exp row per proxy and query head
+    n1 = nacl.workspace_bytes(_prob())
+    p4 = _prob()
+    p4.c.q_group = 4
+    assert nacl.workspace_bytes(p4) > n1
