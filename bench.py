@@ -33,8 +33,8 @@ F32_PEAK_TFLOPS = 157.3        # dense fp32 MFMA
 # (FETCH_SIZE, then WRITE_SIZE) scaled by the same counters on a plain copy of
 # known size; summarised under profiles/.  It is reported only while the
 # kernel source hashes to the value it was measured on.
-MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_split_kernel", "bytes_per_launch": 2206593396,
-                    "source_sha": "8f1e00679359a974"}
+MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_split_kernel", "bytes_per_launch": 2213654203,
+                    "source_sha": "b929c07e3b393f98"}
 
 
 def _source_sha(rel):
@@ -63,6 +63,9 @@ def parse():
                     help="run one kernel three times on layer 0 and exit (for rocprofv3 counter runs)")
     ap.add_argument("--pass-breakdown", action="store_true",
                     help="also time the score kernel's second pass alone (caller-supplied LSE)")
+    ap.add_argument("--generation", action="store_true",
+                    help="instead of the benchmark, time generation-phase re-eviction at decode shapes "
+                         "(append m rows, evict the C + m cache back to C in place)")
     ap.add_argument("--configs", action="store_true",
                     help="instead of the benchmark, print one JSON line per parity workload (GPU times, "
                          "score roofline fraction, oracle rate on a bounded sample of heads)")
@@ -84,6 +87,9 @@ def main():
 
     if args.configs:
         run_configs()
+        return
+    if args.generation:
+        run_generation(args.workload)
         return
     w = WORKLOADS[args.workload]
     layers = args.layers or w.layers
@@ -244,6 +250,74 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def run_generation(name, m_steps=(16, 64, 256)):
+    """Generation-phase eviction (Section 3; Algorithm 1, Generation) at decode
+    shapes: the cache of one layer holds C kept entries per head plus m decoding
+    steps; a round appends the m new K/V rows (nacl_append) and evicts the
+    C + m cache back to C in place with the current token as the only proxy.
+    Events around ten back-to-back rounds, median of three such runs; one JSON
+    line per m."""
+    import statistics
+    import torch
+    from paper_2408_03675_amd import nacl
+    from synth import WORKLOADS
+
+    w = WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    nacl.load_library()
+    g = torch.Generator(device=dev).manual_seed(5)
+    dt = w.torch_dtype()
+    for m in m_steps:
+        L = w.C + m
+        kc = torch.randn((w.B, w.H, L, w.D), generator=g, device=dev).to(dt)
+        vc = torch.randn((w.B, w.H, L, w.D), generator=g, device=dev).to(dt)
+        k_new = torch.randn((w.B, w.H, m, w.D), generator=g, device=dev).to(dt)
+        v_new = torch.randn((w.B, w.H, m, w.D), generator=g, device=dev).to(dt)
+        q_cur = torch.randn((w.B, w.H, 1, w.D), generator=g, device=dev).to(dt).expand(w.B, w.H, L, w.D)
+        pos_dev = torch.tensor([L - 1], dtype=torch.int32, device=dev)
+        prob = nacl.Problem.from_tensors(q_cur, kc, vc, [L - 1], n_protect=1, proxy_pos_dev=pos_dev)
+        ws = nacl.workspace(prob, dev)
+        F = torch.empty((w.B, w.H, L), dtype=torch.float32, device=dev)
+        keep = torch.empty((w.B, w.H, w.C), dtype=torch.int32, device=dev)
+        Cr = w.Cr
+        stream = torch.cuda.current_stream(dev)
+
+        def rnd(seed):
+            nacl.append(prob, kc, vc, w.C, k_new, v_new)
+            nacl.evict(prob, q_cur, kc, vc, w.C, Cr, nacl.SAMPLE_SOFTMAX, seed, 0, ws=ws, scores=F,
+                       keep_idx=keep, in_place=True)
+
+        def evict_only(seed):
+            nacl.evict(prob, q_cur, kc, vc, w.C, Cr, nacl.SAMPLE_SOFTMAX, seed, 0, ws=ws, scores=F,
+                       keep_idx=keep, in_place=True)
+
+        def med(fn, reps=10, rounds=3):
+            for i in range(3):
+                fn(i)
+            ts = []
+            for r in range(rounds):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for i in range(reps):
+                    fn(100 + r * reps + i)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3 / reps)
+            return statistics.median(ts)
+        t_round = med(rnd)
+        t_evict = med(evict_only)
+        if nacl.health(ws)[1]:
+            raise RuntimeError("a kernel reported a health bit during the generation rounds")
+        print(json.dumps({"metric": "generation-phase re-eviction round", "workload": name, "B": w.B, "H": w.H,
+                          "D": w.D, "dtype": w.dtype, "C": w.C, "Cr": Cr, "m": m, "cache_rows": L,
+                          "round_us": round(t_round, 2), "evict_in_place_us": round(t_evict, 2),
+                          "append_us": round(t_round - t_evict, 2),
+                          "us_per_decoding_step": round(t_round / m, 3)}), flush=True)
+        del kc, vc, k_new, v_new, F, keep, ws
+        torch.cuda.empty_cache()
 
 
 def run_probe(which, w, prob, ws, layer0, out0):

@@ -26,21 +26,28 @@ __device__ __forceinline__ void flag_bad_index(uint32_t* health) {
   }
 }
 
+// VPR: 16-byte vectors per row (D * element size / 16), a compile-time
+// constant so the row and vector of a thread are shifts, not divisions.
+template <int VPR>
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(CompactLaunch a) {
   const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
-  const int vpr = a.row_vecs;
+  constexpr int vpr = VPR;
   const int r = blockIdx.x * (kCompactThreads / vpr) + (int)threadIdx.x / vpr;
   if (r >= a.C) return;
   const int vec = threadIdx.x % vpr;
   const bool is_v = blockIdx.z != 0;
   const int64_t* st = is_v ? a.vs : a.ks;
   const int j = a.keep[(int64_t)bh * a.C + r];
-  u32x4 x = u32x4{0u, 0u, 0u, 0u};
-  if ((unsigned)j < (unsigned)a.L) {
-    const u32x4* src = static_cast<const u32x4*>(is_v ? a.v : a.k) + b * st[0] + h * st[1] + j * st[2] + vec;
-    x = __builtin_nontemporal_load(src);
-  } else if (vec == 0) {
-    flag_bad_index(a.health);
+  // The load is unconditional (an out-of-range index reads row 0 of the
+  // head) so it issues as soon as the index arrives; its value is replaced
+  // by zeros afterwards.
+  const bool ok = (unsigned)j < (unsigned)a.L;
+  const u32x4* src = static_cast<const u32x4*>(is_v ? a.v : a.k) + b * st[0] + h * st[1] +
+                     (int64_t)(ok ? j : 0) * st[2] + vec;
+  u32x4 x = __builtin_nontemporal_load(src);
+  if (!ok) {
+    x = u32x4{0u, 0u, 0u, 0u};
+    if (vec == 0) flag_bad_index(a.health);
   }
   u32x4* dst = static_cast<u32x4*>(is_v ? a.v_out : a.k_out) + ((int64_t)bh * a.C + r) * vpr + vec;
   __builtin_nontemporal_store(x, dst);
@@ -55,14 +62,15 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(CompactLaunch 
 // row may be the destination of another row of the same chunk.  Rows with
 // keep[c] == c stay where they are.
 constexpr int kInplaceThreads = 1024;
-constexpr int kInplaceVecs = 4;  // vectors per thread and chunk
+constexpr int kInplaceVecs = 16;  // vectors per thread and chunk (all loads in flight at once)
 
+template <int VPR>
 __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(CompactLaunch a) {
   const int bh = blockIdx.x, b = bh / a.H, h = bh % a.H;
   const bool is_v = blockIdx.y != 0;
   const int64_t* st = is_v ? a.vs : a.ks;
   u32x4* base = static_cast<u32x4*>(is_v ? a.v_out : a.k_out) + b * st[0] + h * st[1];
-  const int vpr = a.row_vecs;
+  constexpr int vpr = VPR;
   const int rows_per_chunk = kInplaceThreads * kInplaceVecs / vpr;
   const int32_t* keep = a.keep + (int64_t)bh * a.C;
   for (int c0 = 0; c0 < a.C; c0 += rows_per_chunk) {
@@ -109,17 +117,30 @@ __global__ __launch_bounds__(kCompactThreads) void append_kernel(AppendLaunch a)
   *dst = *src;
 }
 
-hipError_t launch_compact(const CompactLaunch& a, hipStream_t stream) {
-  if (a.C == 0) return hipSuccess;
-  if (a.row_vecs <= 0 || kCompactThreads % a.row_vecs != 0) return hipErrorInvalidValue;
+namespace {
+
+template <int VPR>
+hipError_t launch_compact_t(const CompactLaunch& a, hipStream_t stream) {
   if (a.in_place) {
-    hipLaunchKernelGGL(compact_inplace_kernel, dim3(a.B * a.H, 2), dim3(kInplaceThreads), 0, stream, a);
+    hipLaunchKernelGGL(compact_inplace_kernel<VPR>, dim3(a.B * a.H, 2), dim3(kInplaceThreads), 0, stream, a);
     return hipGetLastError();
   }
-  const int rows_per_block = kCompactThreads / a.row_vecs;
+  constexpr int rows_per_block = kCompactThreads / VPR;
   dim3 grid((a.C + rows_per_block - 1) / rows_per_block, a.B * a.H, 2);
-  hipLaunchKernelGGL(compact_kernel, grid, dim3(kCompactThreads), 0, stream, a);
+  hipLaunchKernelGGL(compact_kernel<VPR>, grid, dim3(kCompactThreads), 0, stream, a);
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_compact(const CompactLaunch& a, hipStream_t stream) {
+  if (a.C == 0) return hipSuccess;
+  switch (a.row_vecs) {  // D in {64, 128} x element size in {2, 4}
+    case 8: return launch_compact_t<8>(a, stream);
+    case 16: return launch_compact_t<16>(a, stream);
+    case 32: return launch_compact_t<32>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_append(const AppendLaunch& a, hipStream_t stream) {
