@@ -113,9 +113,12 @@ size_t nacl_workspace_bytes(const nacl_problem* p);
  * so it covers every call since the caller last zeroed it (zero it when the
  * workspace is allocated; the Python binding does).  Bit 0: a wave gave up
  * waiting for a head's log-sum-exp after its bounded spin.  Bit 2 (evict
- * only): the compaction met a keep index outside [0, L).  Never expected;
- * whenever a call's word is non-zero once the stream has completed it, that
- * call's scores, keep_idx, k_out and v_out are not valid. */
+ * only): the compaction met a keep index outside [0, L).  Bit 3 (evict only,
+ * heads of more than 32768 tokens): a work-group of the selection gave up
+ * waiting for the other slices of its head, or its search for a threshold
+ * ran out of rounds.  Never expected; whenever a call's word is non-zero once
+ * the stream has completed it, that call's scores, keep_idx, k_out and v_out
+ * are not valid. */
 int nacl_score(const nacl_problem* p, const void* q, const void* k, const float* lse,
                float* scores, void* ws, size_t ws_bytes, void* stream);
 
