@@ -9,13 +9,16 @@
 //   keep     Pi | u_score | u_random, ascending, exactly C entries
 //
 // Keys are order-preserving uint32 images of the binary32 values (0 marks a
-// token that is not a candidate).  A head of L tokens is cut into slices of
-// kSelSlice tokens, one work-group each, every thread holding kSelPer
-// consecutive tokens in registers; the work-groups of a head exchange data
-// through the workspace in rounds (publish, count one arrival on the head's
-// counter, wait for the other slices), and every work-group takes the same
-// decisions from the same published data.
+// token that is not a candidate).  Heads of up to kRegMaxL tokens take one
+// work-group each, every thread holding 32 tokens' keys in registers
+// (select_kernel_regs, described with it below).  Longer heads are cut into
+// slices of kSelSlice tokens, one work-group each, every thread holding
+// kSelPer consecutive tokens in registers; the work-groups of a head exchange
+// data through the workspace in rounds (publish, count one arrival on the
+// head's counter, wait for the other slices), and every work-group takes the
+// same decisions from the same published data.
 //
+// Sliced heads:
 // Top-k of one key set (k-th largest key T, and `need`, how many keys equal
 // to T belong to the top k; ties go to the lowest indices):
 //   1. pivots: the keys of about kSelSamples sampled tokens (every st-th
@@ -46,6 +49,8 @@
 namespace nacl {
 
 constexpr int kSelWaves = kSelThreads / kWave;
+// Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data format).
+constexpr int kSelBufferRsrcWord3 = 0x00020000;
 
 // Calls f(std::integral_constant<int, i>) for i = 0 .. N-1.
 template <int N, int I = 0, class F>
@@ -138,363 +143,468 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scan_buf) {
 
 
 // ===========================================================================
-// Heads of up to kRegMaxL tokens: one work-group per head, keys in registers.
+// Heads of up to kRegMaxL tokens: one work-group per head.
 //
-// Both top-k searches are exact radix selects over the order-preserving keys
-// (12-, 12- and 8-bit digits, most significant first): each digit pass builds
-// a histogram of the keys that still match the chosen prefix and picks the
-// digit where the count from the top reaches k.  That yields the k-th largest
-// key T and how many keys equal to T to take; a block-wide ordered scan then
-// hands those to the lowest indices.  Set membership lives in LDS bitmaps, one
-// bit per token.
+// Thread t holds the keys of the 32 consecutive tokens 32 t .. 32 t + 31 in
+// registers.  Each key set (scores, then Gumbel keys) is staged in LDS by
+// direct buffer->LDS loads (contiguous 16-byte pieces per lane) and read
+// back as eight 16-byte pieces per thread in the rotated order (q + t) mod 8,
+// under which the eight lanes an LDS cycle serves touch distinct banks; so
+// register slot i holds token 32 t + ((i + 4 t) mod 32), and a mask over the
+// slots is a mask over the thread's tokens rotated by 4 t.  The Gumbel keys
+// are loaded into the staging buffer while the scores are searched.
+// Top-k of one key set (the k-th largest key T, and `need`, how many keys
+// equal to T the top k holds; ties go to the lower index):
+//   1. window: one sampled key per thread (a different slot in each thread,
+//      so the sample spans the head) goes into a histogram of its top 12
+//      bits; the bins holding the sample's ranks k*m/n -/+ three standard
+//      deviations give a window [lo, hi) that holds the k-th largest key in
+//      all likelihood.  The largest key M is reduced at the same time;
+//   2. every key at or above lo is counted in 4095 equal bins of width 2^sh
+//      covering [lo, min(hi, M + 1)), plus one bin for everything above, and
+//      the bin holding the k-th largest key is picked: its keys share all
+//      bits at and above sh;
+//   3. when every key of that bin is taken, "key >= the bin's lower edge"
+//      is the top k; otherwise a bin of at most kRegCand keys is gathered and
+//      ranked in one wave, and a larger one takes radix passes over the bits
+//      below sh.  When the window misses the k-th key, a plain radix select
+//      (12-, 12- and 8-bit digits) over all keys runs instead.
+// Each histogram is read by one wave (64 bins per lane, a wave scan over the
+// lanes, then one bin per lane inside the crossing lane's range), so a pass
+// costs two barriers.  Membership is then a register compare, with a block
+// scan of the per-thread counts of keys equal to T when only some of them
+// are taken.  Assembly scans the per-thread counts of kept tokens, and every
+// thread stores its kept indices in order at the offset the scan gives.
 
-struct SelScratch {
-  uint32_t* hist;   // kHistBins, all zero between radix passes
-  uint32_t* scan;   // 2 * kSelWaves
-  uint32_t* shv;    // 3: radix pick results
-};
-
-// Radix select digits, most significant first: 12 + 12 + 8 bits.  The wide
-// first digit spreads even tightly clustered keys (scores within a few
-// binades) over many counters, so the shared histogram's atomics rarely
-// collide; later passes only count keys that match the chosen prefix.
-constexpr int kHistBins = 4096;
-constexpr int kDigitShift[3] = {20, 8, 0};
-constexpr int kDigitBits[3] = {12, 12, 8};
-
-// After a histogram pass over the digit at `shift`: the digit at which the
-// count from the top reaches kr, appended to prefix; kr becomes the rank
-// within that digit's keys and n_eq their number.  Thread t owns bins
-// nbins-1-per*t down to nbins-per-per*t and zeroes them once read, so the
-// histogram is all zero again for the next pass.
-__device__ void radix_pick(int shift, int nbins, const SelScratch& s, uint32_t& prefix, uint32_t& kr,
-                           uint32_t& n_eq) {
-  const int tid = threadIdx.x;
-  const int per = (nbins + kSelThreads - 1) / kSelThreads;  // 4 or 1
-  uint32_t c[4] = {0u, 0u, 0u, 0u}, local = 0u;
-#pragma unroll
-  for (int qq = 0; qq < 4; ++qq) {
-    const int b = nbins - 1 - per * tid - qq;
-    if (qq < per && b >= 0) {
-      c[qq] = s.hist[b];
-      s.hist[b] = 0u;
-    }
-    local += c[qq];
-  }
-  const uint32_t excl = block_exclusive_scan(local, s.scan);
-  if (excl < kr && kr <= excl + local) {
-    uint32_t cum = excl;
-    for (int qq = 0; qq < per; ++qq) {
-      if (cum + c[qq] >= kr) {
-        s.shv[0] = prefix | ((uint32_t)(nbins - 1 - per * tid - qq) << shift);
-        s.shv[1] = kr - cum;
-        s.shv[2] = c[qq];
-        break;
-      }
-      cum += c[qq];
-    }
-  }
-  // The next write of shv follows the next pass's histogram barrier, which
-  // every thread reaches only after reading these values.
-  __syncthreads();
-  prefix = s.shv[0];
-  kr = s.shv[1];
-  n_eq = s.shv[2];
-}
-
-// k-th largest key T (1 <= k <= number of keys), the number `need` of keys
-// equal to T that belong to the top k, and the number n_eq of keys equal to T.
-// get(j) reads key j.  A key of 0 marks an excluded token and is never
-// counted: the first pass skips it, and later prefixes never match it (an
-// order key below 2^20 would be a NaN, so every real key has a nonzero
-// first digit).
-template <class Get>
-__device__ void radix_select(const Get& get, int L, uint32_t k, const SelScratch& s, uint32_t& T,
-                             uint32_t& need, uint32_t& n_eq) {
-  const int tid = threadIdx.x;
-  uint32_t prefix = 0u, kr = k;
-#pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = kDigitShift[pass];
-    const uint32_t dmask = (1u << kDigitBits[pass]) - 1u;
-    const uint32_t hm = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + kDigitBits[pass]));
-    // Eight keys per thread in flight before their counter updates.
-    for (int j0 = tid; j0 < L; j0 += 8 * kSelThreads) {
-      uint32_t kv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 + u * kSelThreads;
-        kv[u] = j < L ? get(j) : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (pass == 0 ? kv[u] != 0u : ((kv[u] ^ prefix) & hm) == 0u)
-          atomicAdd(&s.hist[(kv[u] >> shift) & dmask], 1u);
-    }
-    __syncthreads();
-    radix_pick(shift, 1 << kDigitBits[pass], s, prefix, kr, n_eq);
-  }
-  T = prefix;
-  need = kr;
-}
-
-// The same over keys held in registers: key[i] belongs to token
-// i * kSelThreads + threadIdx.x (0 past the end of the head or excluded).
-template <int NR>
-__device__ __forceinline__ void radix_select_regs(const uint32_t (&key)[NR], uint32_t k, const SelScratch& s,
-                                                  uint32_t& T, uint32_t& need, uint32_t& n_eq) {
-  uint32_t prefix = 0u, kr = k;
-#pragma unroll
-  for (int pass = 0; pass < 3; ++pass) {
-    const int shift = kDigitShift[pass];
-    const uint32_t dmask = (1u << kDigitBits[pass]) - 1u;
-    const uint32_t hm = pass == 0 ? 0u : (0xFFFFFFFFu << (shift + kDigitBits[pass]));
-#pragma unroll
-    for (int i = 0; i < NR; ++i)
-      if (pass == 0 ? key[i] != 0u : ((key[i] ^ prefix) & hm) == 0u)
-        atomicAdd(&s.hist[(key[i] >> shift) & dmask], 1u);
-    __syncthreads();
-    radix_pick(shift, 1 << kDigitBits[pass], s, prefix, kr, n_eq);
-  }
-  T = prefix;
-  need = kr;
-}
-
-// Sets, in out_bits, the bit of every token with key >= T (T > 0): the top k
-// when every key equal to T belongs to it.  Each wave covers 64 consecutive
-// tokens per step; lanes 0 and 32 OR the two words of the ballot into the
-// bitmap with LDS atomics that return nothing (no wait on the old word), and
-// the four steps of an iteration keep their loads and updates independent.
-template <class Get>
-__device__ void mark_at_least(const Get& get, int L, uint32_t T, uint32_t* out_bits) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int b0 = wave * 64; b0 < L; b0 += 4 * kSelThreads) {
-    bool take[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int j = b0 + u * kSelThreads + lane;
-      take[u] = j < L && get(j) >= T;
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int base = b0 + u * kSelThreads;
-      const uint64_t m = __ballot(take[u]);
-      const int word = (base >> 5) + (lane >> 5);
-      if ((lane & 31) == 0 && base + (lane & 32) < L) {
-        const uint32_t bits = (lane & 32) ? (uint32_t)(m >> 32) : (uint32_t)m;
-        if (bits) atomicOr(&out_bits[word], bits);
-      }
-    }
-  }
-  __syncthreads();
-}
-
-// The same over keys in registers (same token mapping as radix_select_regs).
-template <int NR>
-__device__ __forceinline__ void mark_at_least_regs(const uint32_t (&key)[NR], int L, uint32_t T, uint32_t* out_bits) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int i = 0; i < NR; ++i) {
-    const int base = i * kSelThreads + wave * 64;
-    const uint64_t m = __ballot(key[i] >= T);
-    if ((lane & 31) == 0 && base + (lane & 32) < L) {
-      const uint32_t bits = (lane & 32) ? (uint32_t)(m >> 32) : (uint32_t)m;
-      if (bits) atomicOr(&out_bits[(base >> 5) + (lane >> 5)], bits);
-    }
-  }
-  __syncthreads();
-}
-
-// Sets, in out_bits, the bit of every token with key > T and of the first
-// `need` tokens (in index order) with key == T.  Thread t owns bitmap words
-// [t * seg_words, (t + 1) * seg_words).
-template <class Get>
-__device__ void mark_top(const Get& get, int L, int nwords, int seg_words, uint32_t T, uint32_t need,
-                         uint32_t* out_bits, uint32_t* scan_buf) {
-  const int w0 = threadIdx.x * seg_words;
-  const int w1 = min(w0 + seg_words, nwords);
-  uint32_t ties = 0;
-  for (int w = w0; w < w1; ++w)
-    for (int bit = 0; bit < 32; ++bit) {
-      const int j = w * 32 + bit;
-      if (j < L && get(j) == T) ++ties;
-    }
-  uint32_t rank = block_exclusive_scan(ties, scan_buf);
-  for (int w = w0; w < w1; ++w) {
-    uint32_t word = 0;
-    for (int bit = 0; bit < 32; ++bit) {
-      const int j = w * 32 + bit;
-      if (j < L) {
-        const uint32_t key = get(j);
-        bool take = key > T;
-        if (key == T) {
-          take = rank < need;
-          ++rank;
-        }
-        if (take) word |= 1u << bit;
-      }
-    }
-    out_bits[w] |= word;
-  }
-  __syncthreads();
-}
-
-// The top k of get() into out_bits: ballot marking when every key equal to
-// the k-th largest is kept, the ordered tie scan otherwise.
-template <class Get>
-__device__ void select_top(const Get& get, int L, int nwords, int seg_words, uint32_t k,
-                           const SelScratch& s, uint32_t* out_bits) {
-  uint32_t T, need, n_eq;
-  radix_select(get, L, k, s, T, need, n_eq);
-  if (need == n_eq) mark_at_least(get, L, T, out_bits);
-  else mark_top(get, L, nwords, seg_words, T, need, out_bits, s.scan);
-}
-
-// keep = the set bits of a | b in ascending order, C of them: ranks by an
-// ordered scan of the bitmap words (thread t owns words [t * seg_words,
-// (t + 1) * seg_words)), the list assembled in `list` (LDS, then copied out
-// with coalesced stores, or keep itself).
-__device__ void assemble_keep(const uint32_t* a_bits, const uint32_t* b_bits, int nwords, int seg_words, int C,
-                              const SelScratch& s, int32_t* list, int32_t* keep) {
-  const int tid = threadIdx.x;
-  const int w0 = tid * seg_words;
-  const int w1 = min(w0 + seg_words, nwords);
-  uint32_t cnt = 0;
-  for (int w = w0; w < w1; ++w) cnt += __popc(a_bits[w] | b_bits[w]);
-  uint32_t out = block_exclusive_scan(cnt, s.scan);
-  for (int w = w0; w < w1; ++w) {
-    uint32_t bits = a_bits[w] | b_bits[w];
-    while (bits) {
-      const int bit = __ffs(bits) - 1;
-      if (out < (uint32_t)C) list[out] = w * 32 + bit;  // |keep| == C by construction
-      ++out;
-      bits &= bits - 1;
-    }
-  }
-  if (list != keep) {
-    __syncthreads();
-    for (int c = tid; c < C; c += kSelThreads) keep[c] = list[c];
-  }
-}
-
-// Heads of up to kRegMaxL tokens: every thread holds the scores and Gumbel
-// keys of tokens tid + i * kSelThreads (i < kRegKeys) in registers, both
-// loaded at the start so the Gumbel keys arrive while the top-Cp search
-// runs.  Radix passes and ballot marking then touch LDS only for the
-// histogram and the bitmaps.  LDS: L words (the keys for the ordered tie
-// scan, then the keep list), two bitmaps, the histogram.
 constexpr int kRegKeys = 32;
 constexpr int kRegMaxL = kRegKeys * kSelThreads;
 static_assert(kRegMaxL == kSelRegMaxL, "register selection length");
+constexpr int kHistBins = 4096;
+static_assert(kHistBins == 64 * kWave, "histogram scan: 64 bins per lane of one wave");
+constexpr int kRegCand = kWave;  // bins resolved by one wave
 
-// The top k of the register keys into out_bits; returns the k-th largest
-// key T when the top k are exactly the keys >= T (then a token's membership
-// is a register compare), else 0 (ties at T split by index).
-template <int NR>
-__device__ __forceinline__ uint32_t top_regs(const uint32_t (&key)[NR], int L, uint32_t k, const SelScratch& s,
-                                             uint32_t* keys_lds, uint32_t* out_bits) {
+// A barrier without the full fence of __syncthreads(): it waits for this
+// wave's LDS operations (so LDS writes before it are seen by every wave after
+// it) but not for its vector memory operations, so the buffer->LDS loads of
+// the Gumbel keys stay in flight across it (a fence would wait for them,
+// since they write LDS).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// LDS atomics written as instructions the compiler does not see as memory
+// accesses: it makes every LDS atomic that follows a buffer->LDS load wait
+// for that load (it cannot tell them apart), which would make the score
+// search wait for the Gumbel keys.  Every LDS location they touch is read
+// only after a barrier (which waits for them), and the LDS counter counts
+// them in issue order, so the compiler's own LDS waits stay sufficient.
+__device__ __forceinline__ uint32_t lds_off(const uint32_t* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint32_t*)p;
+}
+__device__ __forceinline__ void lds_add(uint32_t* p, uint32_t v) {
+  asm volatile("ds_add_u32 %0, %1" ::"v"(lds_off(p)), "v"(v));
+}
+__device__ __forceinline__ void lds_or(uint32_t* p, uint32_t v) {
+  asm volatile("ds_or_b32 %0, %1" ::"v"(lds_off(p)), "v"(v));
+}
+__device__ __forceinline__ void lds_max(uint32_t* p, uint32_t v) {
+  asm volatile("ds_max_u32 %0, %1" ::"v"(lds_off(p)), "v"(v));
+}
+// Returns the old value (waits for it).
+__device__ __forceinline__ uint32_t lds_add_rtn(uint32_t* p, uint32_t v) {
+  uint32_t r;
+  asm volatile("ds_add_rtn_u32 %0, %1, %2\n\ts_waitcnt lgkmcnt(0)" : "=v"(r) : "v"(lds_off(p)), "v"(v));
+  return r;
+}
+
+struct RegLds {
+  alignas(16) uint32_t hist[kHistBins];  // all zero between passes
+  uint32_t fixed[kRegMaxL / 32];         // Pi, one bit per token (word t: tokens 32 t ..)
+  uint32_t cand[kRegCand];               // keys of the k-th bin (step 3)
+  uint32_t pick[2][4];                   // per rank: found, bin, rank within the bin, bin count
+  uint32_t scan[2 * kSelWaves];
+  uint32_t shv[8];                       // 0-2 ranked result, 4 gather counter, 5 max key, 6 valid samples
+};
+
+struct TopK {
   uint32_t T, need, n_eq;
-  radix_select_regs(key, k, s, T, need, n_eq);
-  if (need == n_eq) {
-    mark_at_least_regs(key, L, T, out_bits);
-    return T;
-  } else {
-#pragma unroll
-    for (int i = 0; i < NR; ++i) {
-      const int j = i * kSelThreads + (int)threadIdx.x;
-      if (j < L) keys_lds[j] = key[i];
-    }
-    __syncthreads();
-    mark_top([&](int j) { return keys_lds[j]; }, L, (L + 31) / 32, 1, T, need, out_bits, s.scan);
-    return 0u;
+};
+
+__device__ __forceinline__ uint32_t rotr32(uint32_t x, uint32_t r) { return __builtin_amdgcn_alignbit(x, x, r); }
+__device__ __forceinline__ uint32_t rotl32(uint32_t x, uint32_t r) { return __builtin_amdgcn_alignbit(x, x, (32u - r) & 31u); }
+
+// Maximum over the wave (the inclusive scan's shifts with max).
+__device__ __forceinline__ uint32_t wave_max(uint32_t x) {
+  x = max(x, dpp_or_zero<0x111, 0xf>(x));
+  x = max(x, dpp_or_zero<0x112, 0xf>(x));
+  x = max(x, dpp_or_zero<0x114, 0xf>(x));
+  x = max(x, dpp_or_zero<0x118, 0xf>(x));
+  x = max(x, dpp_or_zero<0x142, 0xa>(x));
+  x = max(x, dpp_or_zero<0x143, 0xc>(x));
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, kWave - 1);
+}
+
+// Exclusive prefix sum of v over the work-group in thread order (the scan of
+// block_exclusive_scan with barriers that leave the buffer->LDS loads in
+// flight).
+__device__ __forceinline__ uint32_t reg_block_scan(uint32_t v, uint32_t* scan_buf) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t x = wave_inclusive_scan(v);
+  if (lane == kWave - 1) scan_buf[wave] = x;
+  lds_barrier();
+  if (wave == 0) {
+    uint32_t t = lane < kSelWaves ? scan_buf[lane] : 0u;
+    t = wave_inclusive_scan(t);
+    if (lane < kSelWaves) scan_buf[kSelWaves + lane] = t;
   }
+  lds_barrier();
+  const uint32_t base = wave ? scan_buf[kSelWaves + wave - 1] : 0u;
+  return base + x - v;
+}
+
+// Sorts the 64 * R keys v[r] of lane l (element l * R + r) of one wave into
+// descending order by a bitonic network in registers: stages within a lane
+// swap registers, stages across lanes exchange with the partner lane.
+template <int R>
+__device__ __forceinline__ void wave_sort_desc(uint32_t (&v)[R]) {
+  const int lane = threadIdx.x & 63;
+  static_for<__builtin_ctz(64 * R)>([&](auto kc) {
+    constexpr int k = 2 << decltype(kc)::value;
+    static_for<decltype(kc)::value + 1>([&](auto jc) {
+      constexpr int j = k >> (1 + decltype(jc)::value);
+      if constexpr (j < R) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if ((r & j) == 0) {
+            const bool desc = ((lane * R + r) & k) == 0;
+            const uint32_t x = v[r], y = v[r | j];
+            v[r] = desc ? max(x, y) : min(x, y);
+            v[r | j] = desc ? min(x, y) : max(x, y);
+          }
+        }
+      } else {
+        constexpr int lm = j / R;  // partner lane = lane ^ lm
+        const bool lower = (lane & lm) == 0;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const bool desc = ((lane * R + r) & k) == 0;
+          const uint32_t y = (uint32_t)__shfl_xor((int)v[r], lm);
+          v[r] = (lower == desc) ? max(v[r], y) : min(v[r], y);
+        }
+      }
+    });
+  });
+}
+
+// Called by every thread once a histogram is complete (after its barrier).
+// For each rank kr[r] (1-based from the top; 0: none), wave 0 finds the bin
+// at which the count from the top reaches it and stores (found, bin, rank
+// within the bin, bin count) in s.pick[r]; it also clears the histogram.
+// Lane l owns bins 4095 - 64 l down to 4032 - 64 l, read and cleared as 16
+// pieces of four bins in the order (q + l) mod 16, so that the eight lanes
+// an LDS cycle serves touch distinct banks.  Ends with a barrier.
+template <int NRK>
+__device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) {
+  if (threadIdx.x < kWave) {
+    const int lane = threadIdx.x;
+    uint4* own = reinterpret_cast<uint4*>(s.hist + kHistBins - 64 * (lane + 1));
+    uint32_t sum = 0u;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const uint4 v = own[(q + lane) & 15];
+      sum += v.x + v.y + v.z + v.w;
+    }
+    const uint32_t incl = wave_inclusive_scan(sum);
+    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+#pragma unroll
+    for (int r = 0; r < NRK; ++r) {
+      const uint32_t want = kr[r];
+      if (want == 0u || want > total) {
+        if (lane == 0) s.pick[r][0] = 0u;
+        continue;
+      }
+      const int l0 = (int)__builtin_ctzll(__ballot(incl >= want));
+      const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)(incl - sum), l0);
+      const int b = kHistBins - 1 - 64 * l0 - lane;  // lane m: the m-th bin of lane l0 from the top
+      const uint32_t c = s.hist[b];
+      const uint32_t inc2 = above + wave_inclusive_scan(c);
+      const int m = (int)__builtin_ctzll(__ballot(inc2 >= want));
+      if (lane == m) {
+        s.pick[r][0] = 1u;
+        s.pick[r][1] = (uint32_t)b;
+        s.pick[r][2] = want - (inc2 - c);
+        s.pick[r][3] = c;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) own[(q + lane) & 15] = uint4{0u, 0u, 0u, 0u};
+  }
+  lds_barrier();
+}
+
+// The kr-th largest of the keys whose bits at and above `bits` equal those
+// of prefix (its lower bits zero; bits == 32: every key), by radix passes of
+// 12 bits (the last one narrower) over the bits below; key 0 never counts.
+// At least kr keys must match.
+template <int NR>
+__device__ __forceinline__ TopK radix_rest(const uint32_t (&key)[NR], RegLds& s, uint32_t prefix, int bits,
+                                           uint32_t kr) {
+  uint32_t n_eq = 0u;
+#pragma unroll 1
+  while (bits > 0) {
+    const int d = bits > 12 ? 12 : bits;
+    const int shift = bits - d;
+    const uint32_t hm = bits >= 32 ? 0u : (0xFFFFFFFFu << bits);
+    const uint32_t dmask = (1u << d) - 1u;
+#pragma unroll
+    for (int i = 0; i < NR; ++i)
+      if (key[i] != 0u && ((key[i] ^ prefix) & hm) == 0u) lds_add(&s.hist[(key[i] >> shift) & dmask], 1u);
+    lds_barrier();
+    const uint32_t want[1] = {kr};
+    pick_bins(s, want);
+    prefix |= s.pick[0][1] << shift;
+    kr = s.pick[0][2];
+    n_eq = s.pick[0][3];
+    bits = shift;
+    lds_barrier();  // pick results read before the next pass rewrites them
+  }
+  return TopK{prefix, kr, n_eq};
+}
+
+// Top k (1 <= k <= number of nonzero keys) of the register keys; n_valid is
+// the number of nonzero keys of the head (it only scales the sample ranks).
+template <int NR>
+__device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k, uint32_t n_valid, RegLds& s) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // 1. One sampled key per thread, and the largest key.
+  uint32_t smp = 0u, vmax = 0u;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    smp = (tid & (NR - 1)) == i ? key[i] : smp;
+    vmax = max(vmax, key[i]);
+  }
+  vmax = wave_max(vmax);
+  const uint64_t sb = __ballot(smp != 0u);
+  if (lane == 0) {
+    lds_max(&s.shv[5], vmax);
+    lds_add(&s.shv[6], (uint32_t)__popcll(sb));
+  }
+  if (smp != 0u) lds_add(&s.hist[smp >> 20], 1u);
+  lds_barrier();
+  const uint32_t M = s.shv[5], n_s = s.shv[6];
+  const float e = (float)k * (float)n_s / (float)n_valid;
+  const float dev = 3.f * sqrtf(e) + 3.f;
+  const uint32_t want[2] = {n_s ? min(n_s, (uint32_t)ceilf(e + dev)) : 0u,
+                            e - dev >= 1.f ? (uint32_t)(e - dev) : 0u};
+  pick_bins(s, want);
+  const bool have_lo = s.pick[0][0] != 0u, have_hi = s.pick[1][0] != 0u;
+  const uint64_t lo = (uint64_t)s.pick[0][1] << 20;
+  const uint64_t hi = have_hi ? min((uint64_t)(s.pick[1][1] + 1u) << 20, (uint64_t)M + 1u) : (uint64_t)M + 1u;
+  lds_barrier();  // pick, maximum and sample count read before they are reused
+  if (tid == 0) {
+    s.shv[4] = 0u;
+    s.shv[5] = 0u;
+    s.shv[6] = 0u;
+  }
+  // Radix passes left to do: over the bits below rbits of the keys matching
+  // rprefix, for the rkr-th largest.
+  uint32_t rprefix = 0u, rkr = k;
+  int rbits = 32;
+  if (have_lo) {
+    // 2. Bins 0..4094 of width 2^sh cover [lo, hi); bin 4095 takes the rest.
+    //    sh <= 20 unless lo == 0, so lo is a multiple of 2^sh.
+    const uint64_t range = hi > lo ? hi - lo : 1u;
+    int sh = 0;
+    while (((uint64_t)(kHistBins - 1) << sh) < range) ++sh;
+    const uint32_t lo32 = (uint32_t)lo, lo_nz = lo32 ? lo32 : 1u;  // key 0 never counts
+#pragma unroll
+    for (int i = 0; i < NR; ++i)
+      if (key[i] >= lo_nz) lds_add(&s.hist[min((key[i] - lo32) >> sh, (uint32_t)(kHistBins - 1))], 1u);
+    lds_barrier();
+    const uint32_t want1[1] = {k};
+    pick_bins(s, want1);
+    const bool found = s.pick[0][0] != 0u && s.pick[0][1] != (uint32_t)(kHistBins - 1);
+    const uint32_t pfx = (lo32 >> sh) + s.pick[0][1];
+    const uint32_t kr = s.pick[0][2], n1 = s.pick[0][3];
+    lds_barrier();  // pick read before it is reused
+    if (found) {
+      // 3. Keys with high bits pfx: the kr-th largest of the n1 of them.
+      if (sh == 0) return TopK{pfx, kr, n1};
+      if (kr == n1) return TopK{pfx << sh, n1, n1};
+      rprefix = pfx << sh;
+      rbits = sh;
+      rkr = kr;
+      if (n1 <= (uint32_t)kRegCand) {
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+          const bool m = key[i] != 0u && (key[i] >> sh) == pfx;
+          if (m) s.cand[lds_add_rtn(&s.shv[4], 1u)] = key[i];
+        }
+        lds_barrier();
+        if (wave == 0) {
+          // Lane l holds candidate l; it counts the candidates above and
+          // equal to its own.  The lanes whose key is the kr-th largest
+          // publish it.
+          const uint32_t v = lane < (int)n1 ? s.cand[lane] : 0u;
+          uint32_t n_gt = 0u, n_eq = 0u;
+          for (int j = 0; j < (int)n1; ++j) {
+            const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, j);
+            n_gt += c > v ? 1u : 0u;
+            n_eq += c == v ? 1u : 0u;
+          }
+          if (lane < (int)n1 && n_gt < kr && kr <= n_gt + n_eq) {
+            s.shv[0] = v;
+            s.shv[1] = kr - n_gt;
+            s.shv[2] = n_eq;
+          }
+          if (lane == 0) s.shv[4] = 0u;
+        }
+        lds_barrier();
+        const TopK r{s.shv[0], s.shv[1], s.shv[2]};
+        lds_barrier();  // read before shv is reused
+        return r;
+      }
+    }
+  }
+  return radix_rest(key, s, rprefix, rbits, rkr);
+}
+
+// Bit i: the token of slot i belongs to the top k described by r (rot: the
+// thread's slot rotation).
+template <int NR>
+__device__ __forceinline__ uint32_t top_members(const uint32_t (&key)[NR], const TopK& r, uint32_t rot,
+                                                RegLds& s) {
+  uint32_t in = 0u;
+  if (r.need == r.n_eq) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) in |= (key[i] >= r.T ? 1u : 0u) << i;
+    return in;
+  }
+  // Only the first `need` keys equal to T, in token order, are taken.
+  uint32_t tie = 0u;
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    in |= (key[i] > r.T ? 1u : 0u) << i;
+    tie |= (key[i] == r.T ? 1u : 0u) << i;
+  }
+  uint32_t t_tok = rotl32(tie, rot);  // token order
+  const uint32_t n = (uint32_t)__popc(t_tok);
+  const uint32_t before = reg_block_scan(n, s.scan);
+  uint32_t take = min(r.need - min(r.need, before), n);  // need - before, or 0 past the need-th tie
+  uint32_t kept_tok = 0u;
+  while (take--) {
+    const uint32_t low = t_tok & (0u - t_tok);
+    kept_tok |= low;
+    t_tok ^= low;
+  }
+  return in | rotr32(kept_tok, rot);
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a) {
-  extern __shared__ uint32_t smem[];
+  __shared__ RegLds s;
+  __shared__ uint32_t stage[kRegMaxL];  // one key set of the head, by buffer->LDS loads
   const int L = a.L;
-  const int nwords = (L + 31) / 32;  // <= kSelThreads
-  uint32_t* keys_lds = smem;
-  uint32_t* fixed = smem + L;        // Pi, then Pi | u_score
-  uint32_t* rnd = fixed + nwords;    // u_random
-  SelScratch s;
-  s.hist = rnd + nwords;
-  s.scan = s.hist + kHistBins;
-  s.shv = s.scan + 2 * kSelWaves;
-
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = blockIdx.x;
-  const uint32_t* fbits = reinterpret_cast<const uint32_t*>(a.scores) + (int64_t)bh * L;
+  const uint32_t* fsrc = reinterpret_cast<const uint32_t*>(a.scores) + (int64_t)bh * L;
   const uint32_t* gsrc = a.keys2 + (int64_t)bh * L;
 
-  // The first protected position is loaded ahead of the keys, so that using
-  // it does not wait for them.
   const int pbase = a.P - a.n_protect;
   const int p0 = pbase + tid < a.P ? a.pos[pbase + tid] : -1;
 
-  // Past the end of the head the loads repeat the last token (masked below),
-  // so every load is unconditional and all of them are in flight at once.
-  uint32_t fk[kRegKeys], gk[kRegKeys];
-  if (a.Cp > 0) {
+  // Stages the head's L words at src in `stage` (reads at or past L, or all
+  // of them when n == 0, return zeros).  Rows that allow it move 16 bytes
+  // per lane: instruction r of wave w moves tokens [256 (16 r + w), + 256).
+  auto stage_keys = [&](const uint32_t* src, int n) {
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(src), (short)0, (int)((uint32_t)n * 4u), kSelBufferRsrcWord3);
+    if ((L & 3) == 0 && ((uintptr_t)src & 15u) == 0) {
 #pragma unroll
-    for (int i = 0; i < kRegKeys; ++i) fk[i] = fbits[min(i * kSelThreads + tid, L - 1)];
-  }
-  if (a.Cr > 0) {
-#pragma unroll
-    for (int i = 0; i < kRegKeys; ++i) gk[i] = gsrc[min(i * kSelThreads + tid, L - 1)];
-  }
-
-  if (tid < nwords) {
-    fixed[tid] = 0u;
-    rnd[tid] = 0u;
-  }
-  for (int i = tid; i < kHistBins; i += kSelThreads) s.hist[i] = 0u;
-  __syncthreads();
-  if (p0 >= 0) atomicOr(&fixed[p0 >> 5], 1u << (p0 & 31));
-  for (int i = pbase + tid + kSelThreads; i < a.P; i += kSelThreads) {
-    const int j = a.pos[i];
-    atomicOr(&fixed[j >> 5], 1u << (j & 31));
-  }
-  __syncthreads();
-  auto is_fixed = [&](int j) -> bool { return ((fixed[j >> 5] >> (j & 31)) & 1u) != 0u; };
-
-  // u_score: top-Cp of F over R = [0, L) \ Pi, marked into `fixed`.
-  uint32_t T1 = 0u;
-  if (a.Cp > 0) {
-#pragma unroll
-    for (int i = 0; i < kRegKeys; ++i) {
-      const int j = i * kSelThreads + tid;
-      fk[i] = (j < L && !is_fixed(j)) ? float_order_key(__uint_as_float(fk[i])) : 0u;
-    }
-    T1 = top_regs(fk, L, (uint32_t)a.Cp, s, keys_lds, fixed);
-  }
-
-  // u_random: top-Cr of the Gumbel keys over R \ u_score.  Excluded are the
-  // tokens past the end, Pi (score key 0) and u_score (score key >= T1)
-  // when u_score is exactly the keys >= T1; otherwise the bitmap says.
-  if (a.Cr > 0) {
-    if (T1) {
-#pragma unroll
-      for (int i = 0; i < kRegKeys; ++i)
-        if (fk[i] == 0u || fk[i] >= T1) gk[i] = 0u;
+      for (int r = 0; r < kRegMaxL / (256 * kSelWaves); ++r) {
+        const uint32_t t0 = 256u * (uint32_t)(kSelWaves * r + wave);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + t0), 16,
+                                                 (t0 + 4u * (uint32_t)lane) * 4u, 0, 0, 0);
+      }
     } else {
 #pragma unroll
-      for (int i = 0; i < kRegKeys; ++i) {
-        const int j = i * kSelThreads + tid;
-        if (j >= L || is_fixed(j)) gk[i] = 0u;
+      for (int r = 0; r < kRegMaxL / (64 * kSelWaves); ++r) {
+        const uint32_t t0 = 64u * (uint32_t)(kSelWaves * r + wave);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + t0), 4,
+                                                 (t0 + (uint32_t)lane) * 4u, 0, 0, 0);
       }
     }
-    top_regs(gk, L, (uint32_t)a.Cr, s, keys_lds, rnd);
+  };
+  // Thread t's 32 staged words, slot i = token 32 t + ((i + rot) mod 32).
+  const uint32_t rot = (4u * (uint32_t)tid) & 31u;
+  uint32_t key[kRegKeys];
+  auto read_stage = [&]() {
+    const uint4* row = reinterpret_cast<const uint4*>(stage + kRegKeys * tid);
+#pragma unroll
+    for (int q = 0; q < kRegKeys / 4; ++q) {
+      const uint4 v = row[(q + tid) & 7];
+      key[4 * q] = v.x;
+      key[4 * q + 1] = v.y;
+      key[4 * q + 2] = v.z;
+      key[4 * q + 3] = v.w;
+    }
+  };
+
+  stage_keys(fsrc, a.Cp > 0 ? L : 0);
+  s.fixed[tid] = 0u;
+#pragma unroll
+  for (int q = 0; q < kHistBins / kSelThreads; ++q) s.hist[q * kSelThreads + tid] = 0u;
+  if (tid < 8) s.shv[tid] = 0u;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's loads
+  lds_barrier();                                    // everyone's, and the clears
+  if (p0 >= 0) lds_or(&s.fixed[p0 >> 5], 1u << (p0 & 31));
+  for (int i = pbase + tid + kSelThreads; i < a.P; i += kSelThreads) {
+    const int j = a.pos[i];
+    lds_or(&s.fixed[j >> 5], 1u << (j & 31));
+  }
+  read_stage();
+  lds_barrier();  // Pi marked; every thread has read the scores
+  // The Gumbel keys arrive while the scores are searched.
+  stage_keys(gsrc, a.Cr > 0 ? L : 0);
+
+  // Bit i of each mask: the token of slot i is in Pi (mp), u_score (ms),
+  // u_random (mr).  Tokens past the end are in none.
+  const int nt = L - kRegKeys * tid;
+  const uint32_t live_tok = nt >= kRegKeys ? 0xFFFFFFFFu : (nt > 0 ? (1u << nt) - 1u : 0u);
+  const uint32_t live = rotr32(live_tok, rot);
+  const uint32_t mp = rotr32(s.fixed[tid], rot);
+  uint32_t ms = 0u, mr = 0u;
+
+  // u_score: top-Cp of F over R = [0, L) \ Pi.
+  if (a.Cp > 0) {
+#pragma unroll
+    for (int i = 0; i < kRegKeys; ++i)
+      key[i] = ((live & ~mp) >> i) & 1u ? float_order_key(__uint_as_float(key[i])) : 0u;
+    const TopK r = reg_top_k(key, (uint32_t)a.Cp, (uint32_t)(L - a.n_protect), s);
+    ms = top_members(key, r, rot, s);
   }
 
-  assemble_keep(fixed, rnd, nwords, 1, a.C, s, reinterpret_cast<int32_t*>(keys_lds), a.keep + (int64_t)bh * a.C);
-}
+  // u_random: top-Cr of the Gumbel keys over R \ u_score.
+  if (a.Cr > 0) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's loads
+    lds_barrier();                                    // everyone's
+    read_stage();
+    const uint32_t cand = live & ~mp & ~ms;
+#pragma unroll
+    for (int i = 0; i < kRegKeys; ++i)
+      if (!((cand >> i) & 1u)) key[i] = 0u;
+    const TopK r = reg_top_k(key, (uint32_t)a.Cr, (uint32_t)(L - a.n_protect - a.Cp), s);
+    mr = top_members(key, r, rot, s);
+  }
 
-
-// LDS bytes of the one-work-group selection for a head of L tokens.
-size_t select_lds_bytes(int L) {
-  const size_t nwords = ((size_t)L + 31) / 32;
-  return ((size_t)L + 2 * nwords + kHistBins + 2 * kSelWaves + 3) * sizeof(uint32_t);
+  // keep = Pi | u_score | u_random in index order: C entries by construction
+  // (the bound only guards the store).
+  uint32_t kept = rotl32(mp | ms | mr, rot);
+  uint32_t o = reg_block_scan((uint32_t)__popc(kept), s.scan);
+  int32_t* out = a.keep + (int64_t)bh * a.C;
+  while (kept) {
+    const int b = __builtin_ctz(kept);
+    if (o < (uint32_t)a.C) out[o] = kRegKeys * tid + b;
+    ++o;
+    kept &= kept - 1u;
+  }
 }
 
 // ===========================================================================
@@ -542,40 +652,6 @@ __device__ __forceinline__ void wave_count(uint32_t* hist, uint32_t bin, bool va
     todo &= ~m;
   }
   if ((todo >> lane) & 1u) atomicAdd(&hist[bin], 1u);
-}
-
-// Sorts the 64 * R keys v[r] of lane l (element l * R + r) of one wave into
-// descending order by a bitonic network in registers: stages within a lane
-// swap registers, stages across lanes exchange with the partner lane.
-template <int R>
-__device__ __forceinline__ void wave_sort_desc(uint32_t (&v)[R]) {
-  const int lane = threadIdx.x & 63;
-  static_for<__builtin_ctz(64 * R)>([&](auto kc) {
-    constexpr int k = 2 << decltype(kc)::value;
-    static_for<decltype(kc)::value + 1>([&](auto jc) {
-      constexpr int j = k >> (1 + decltype(jc)::value);
-      if constexpr (j < R) {
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          if ((r & j) == 0) {
-            const bool desc = ((lane * R + r) & k) == 0;
-            const uint32_t x = v[r], y = v[r | j];
-            v[r] = desc ? max(x, y) : min(x, y);
-            v[r | j] = desc ? min(x, y) : max(x, y);
-          }
-        }
-      } else {
-        constexpr int lm = j / R;  // partner lane = lane ^ lm
-        const bool lower = (lane & lm) == 0;
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-          const bool desc = ((lane * R + r) & k) == 0;
-          const uint32_t y = (uint32_t)__shfl_xor((int)v[r], lm);
-          v[r] = (lower == desc) ? max(v[r], y) : min(v[r], y);
-        }
-      }
-    });
-  });
 }
 
 // The k-th largest (1 <= k <= n) of the n keys in s.a, by four 8-bit radix
@@ -1053,13 +1129,7 @@ hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
     if (e != hipSuccess) return e;
   }
   if (a.L <= kRegMaxL) {
-    const size_t lds = select_lds_bytes(a.L);
-    if (lds > 64 * 1024) {
-      hipError_t e = hipFuncSetAttribute((const void*)select_kernel_regs, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         (int)lds);
-      if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(select_kernel_regs, dim3(BH), dim3(kSelThreads), lds, stream, a);
+    hipLaunchKernelGGL(select_kernel_regs, dim3(BH), dim3(kSelThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.nb < 1 || a.nb > kSelMaxSlices || (int64_t)a.nb * kSelSlice < a.L) return hipErrorInvalidValue;
