@@ -208,6 +208,12 @@ __device__ __forceinline__ void lds_or(uint32_t* p, uint32_t v) {
 __device__ __forceinline__ void lds_max(uint32_t* p, uint32_t v) {
   asm volatile("ds_max_u32 %0, %1" ::"v"(lds_off(p)), "v"(v));
 }
+// Clears 16 bytes (the compiler also makes LDS stores it cannot tell apart
+// from the buffer->LDS loads wait for them).
+__device__ __forceinline__ void lds_zero16(uint32_t* p) {
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  asm volatile("ds_write_b128 %0, %1" ::"v"(lds_off(p)), "v"(z));
+}
 // Returns the old value (waits for it).
 __device__ __forceinline__ uint32_t lds_add_rtn(uint32_t* p, uint32_t v) {
   uint32_t r;
@@ -335,7 +341,7 @@ __device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) 
       }
     }
 #pragma unroll
-    for (int q = 0; q < 16; ++q) own[(q + lane) & 15] = uint4{0u, 0u, 0u, 0u};
+    for (int q = 0; q < 16; ++q) lds_zero16(reinterpret_cast<uint32_t*>(own + ((q + lane) & 15)));
   }
   lds_barrier();
 }
@@ -363,8 +369,7 @@ __device__ __forceinline__ TopK radix_rest(const uint32_t (&key)[NR], RegLds& s,
     prefix |= s.pick[0][1] << shift;
     kr = s.pick[0][2];
     n_eq = s.pick[0][3];
-    bits = shift;
-    lds_barrier();  // pick results read before the next pass rewrites them
+    bits = shift;  // s.pick is next written after the next histogram's barrier
   }
   return TopK{prefix, kr, n_eq};
 }
@@ -374,13 +379,12 @@ __device__ __forceinline__ TopK radix_rest(const uint32_t (&key)[NR], RegLds& s,
 template <int NR>
 __device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k, uint32_t n_valid, RegLds& s) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // 1. One sampled key per thread, and the largest key.
-  uint32_t smp = 0u, vmax = 0u;
+  // 1. One sampled key per thread (slot 0, whose token offset rotates from
+  // thread to thread), and the largest key.
+  const uint32_t smp = key[0];
+  uint32_t vmax = 0u;
 #pragma unroll
-  for (int i = 0; i < NR; ++i) {
-    smp = (tid & (NR - 1)) == i ? key[i] : smp;
-    vmax = max(vmax, key[i]);
-  }
+  for (int i = 0; i < NR; ++i) vmax = max(vmax, key[i]);
   vmax = wave_max(vmax);
   const uint64_t sb = __ballot(smp != 0u);
   if (lane == 0) {
@@ -398,7 +402,8 @@ __device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k,
   const bool have_lo = s.pick[0][0] != 0u, have_hi = s.pick[1][0] != 0u;
   const uint64_t lo = (uint64_t)s.pick[0][1] << 20;
   const uint64_t hi = have_hi ? min((uint64_t)(s.pick[1][1] + 1u) << 20, (uint64_t)M + 1u) : (uint64_t)M + 1u;
-  lds_barrier();  // pick, maximum and sample count read before they are reused
+  // Every thread read the maximum and the sample count before pick_bins's
+  // barrier; s.pick is next written after the next histogram's barrier.
   if (tid == 0) {
     s.shv[4] = 0u;
     s.shv[5] = 0u;
@@ -424,7 +429,6 @@ __device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k,
     const bool found = s.pick[0][0] != 0u && s.pick[0][1] != (uint32_t)(kHistBins - 1);
     const uint32_t pfx = (lo32 >> sh) + s.pick[0][1];
     const uint32_t kr = s.pick[0][2], n1 = s.pick[0][3];
-    lds_barrier();  // pick read before it is reused
     if (found) {
       // 3. Keys with high bits pfx: the kr-th largest of the n1 of them.
       if (sh == 0) return TopK{pfx, kr, n1};
@@ -458,9 +462,8 @@ __device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k,
           if (lane == 0) s.shv[4] = 0u;
         }
         lds_barrier();
-        const TopK r{s.shv[0], s.shv[1], s.shv[2]};
-        lds_barrier();  // read before shv is reused
-        return r;
+        // shv[0..2] are next written after several more barriers.
+        return TopK{s.shv[0], s.shv[1], s.shv[2]};
       }
     }
   }
@@ -561,7 +564,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
   }
   read_stage();
   lds_barrier();  // Pi marked; every thread has read the scores
-  // The Gumbel keys arrive while the scores are searched.
+  // The Gumbel keys arrive while the scores are searched.  (Without random
+  // tokens the loads read nothing and write zeros; they are issued anyway,
+  // which keeps the compiler's wait counts the same on every path.)
   stage_keys(gsrc, a.Cr > 0 ? L : 0);
 
   // Bit i of each mask: the token of slot i is in Pi (mp), u_score (ms),
@@ -595,16 +600,21 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
   }
 
   // keep = Pi | u_score | u_random in index order: C entries by construction
-  // (the bound only guards the store).
+  // (the bound only guards the write).  The list is assembled in the staging
+  // buffer (every thread has read the Gumbel keys from it before the last
+  // selection's barriers), then copied out with coalesced stores.
   uint32_t kept = rotl32(mp | ms | mr, rot);
-  uint32_t o = reg_block_scan((uint32_t)__popc(kept), s.scan);
-  int32_t* out = a.keep + (int64_t)bh * a.C;
+  if (a.Cr == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the zero loads into the buffer
+  uint32_t o = reg_block_scan((uint32_t)__popc(kept), s.scan);  // (its barriers: everyone's)
   while (kept) {
     const int b = __builtin_ctz(kept);
-    if (o < (uint32_t)a.C) out[o] = kRegKeys * tid + b;
+    if (o < (uint32_t)a.C) stage[o] = (uint32_t)(kRegKeys * tid + b);
     ++o;
     kept &= kept - 1u;
   }
+  lds_barrier();
+  int32_t* out = a.keep + (int64_t)bh * a.C;
+  for (int c = tid; c < a.C; c += kSelThreads) out[c] = (int32_t)stage[c];
 }
 
 // ===========================================================================
