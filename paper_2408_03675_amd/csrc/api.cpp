@@ -52,7 +52,7 @@ int q_group_of(const nacl_problem* p) { return p->q_group > 1 ? p->q_group : 1; 
 int rows_of(const nacl_problem* p) { return p->P * q_group_of(p); }
 
 struct Layout {
-  size_t cnt, pos, lse, part, keys, samples, rounds, mid, total;
+  size_t cnt, pos, lse, part, keys, xhist, xcand, total;
   int n_chunks;
   size_t sel_sync_word;   // first word of the selection's sync region inside the counter section
   int n_counter_words;    // counter words cleared before the score kernel (all but the sticky word)
@@ -80,16 +80,14 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up(BH * l.n_chunks * rows * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
-  // The sliced selection of long heads exchanges samples, counts and
-  // candidate lists through these.
+  // The sliced selection of long heads exchanges histograms and candidate
+  // lists through these.
   const bool sliced = nacl::select_uses_slices(p->L);
   const size_t nb = nacl::select_slices(p->L);
-  l.samples = off;
-  if (sliced) off += align_up(BH * 2 * nacl::select_sample_slots(p->L) * sizeof(uint32_t));
-  l.rounds = off;
-  if (sliced) off += align_up(BH * 2 * nb * 2 * sizeof(uint32_t));
-  l.mid = off;
-  if (sliced) off += align_up(BH * 2 * nb * nacl::select_cap_block(p->L) * 2 * sizeof(uint32_t));
+  l.xhist = off;
+  if (sliced) off += align_up(BH * 2 * nb * nacl::kSelHistWords * sizeof(uint32_t));
+  l.xcand = off;
+  if (sliced) off += align_up(BH * 2 * nacl::kSelCandMax * 2 * sizeof(uint32_t));
   l.total = off;
   return l;
 }
@@ -295,13 +293,10 @@ int run_select(const nacl_problem* p, const float* scores, int32_t C, int32_t Cr
   s.keep = keep;
   s.keys_ready = keys_ready ? 1 : 0;
   s.nb = nacl::select_slices(p->L);
-  s.ms = nacl::select_sample_slots(p->L);
-  s.cap_b = nacl::select_cap_block(p->L);
   uint32_t* words = reinterpret_cast<uint32_t*>(ws + l.cnt);
   s.sync = words + l.sel_sync_word;
-  s.samples = reinterpret_cast<uint32_t*>(ws + l.samples);
-  s.rounds = reinterpret_cast<uint32_t*>(ws + l.rounds);
-  s.mid = reinterpret_cast<uint32_t*>(ws + l.mid);
+  s.xhist = reinterpret_cast<uint32_t*>(ws + l.xhist);
+  s.xcand = reinterpret_cast<uint32_t*>(ws + l.xcand);
   s.health = words + 1;
   s.zero_sync = !sync_zeroed;
   hipError_t e = nacl::launch_select(s, stream);

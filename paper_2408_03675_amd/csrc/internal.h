@@ -97,23 +97,20 @@ struct ScoreLaunch {
 
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream);
 
-// Selection: each head is cut into slices of kSelSlice tokens, one
-// work-group per slice (kSelPer consecutive tokens per thread); the slices of
-// a head exchange counts and candidate lists through the workspace.
+// Selection: heads of up to kSelRegMaxL tokens take one work-group each;
+// longer heads are cut into slices of kSelSlice tokens, one work-group per
+// slice (kSelPer consecutive tokens per thread), and the slices of a head
+// exchange histograms and candidate lists through the workspace.
 constexpr int kSelThreads = 1024;
 constexpr int kSelPer = 16;
 constexpr int kSelSlice = kSelThreads * kSelPer;
 constexpr int kSelMaxSlices = (1 << 19) / kSelSlice;   // NACL_MAX_L / kSelSlice
-constexpr int kSelCapBlock = 4096;   // window candidates one slice publishes per round
-constexpr int kSelCapTotal = 16384;  // window candidates the exact step takes
-constexpr int kSelSamples = 512;     // sampled tokens per head (at most)
+constexpr int kSelHistWords = 4096 + 64;               // a slice's published bins and group totals
+constexpr int kSelCandMax = 256;                       // bin keys ranked by every work-group
 __host__ __device__ inline int select_slices(int L) { return (L + kSelSlice - 1) / kSelSlice; }
 // Heads up to this length take the one-work-group kernel (keys in registers).
 constexpr int kSelRegMaxL = 32 * kSelThreads;
 inline bool select_uses_slices(int L) { return L > kSelRegMaxL; }
-__host__ __device__ inline int select_sample_stride(int L) { return (L + kSelSamples - 1) / kSelSamples; }
-__host__ __device__ inline int select_sample_slots(int L) { return L < kSelSamples ? L : kSelSamples; }
-__host__ __device__ inline int select_cap_block(int L) { return L < kSelCapBlock ? L : kSelCapBlock; }
 
 struct SelectLaunch {
   int B, H, L, P, n_protect, C, Cp, Cr, sampling;
@@ -125,12 +122,9 @@ struct SelectLaunch {
   int32_t* keep;         // [B*H, C]
   int keys_ready;        // 1: keys2 already holds the Gumbel keys (drawn by the score kernel)
   int nb;                // slices per head
-  int ms;                // sample slots per head and key: min(L, kSelSamples)
-  int cap_b;             // window candidates per slice and round: min(L, kSelCapBlock)
   uint32_t* sync;        // workspace: word 0 ticket, then (from word 64) one round counter per head; zero at launch
-  uint32_t* samples;     // workspace [B*H, 2, ms]: sampled (score key, Gumbel key)
-  uint32_t* rounds;      // workspace [B*H, 2, nb, 2]: per-round counts of each slice
-  uint32_t* mid;         // workspace [B*H, 2, nb, cap_b, 2]: per-round window candidates
+  uint32_t* xhist;       // workspace [B*H, 2, nb, kSelHistWords]: each slice's bins per round (by parity)
+  uint32_t* xcand;       // workspace [B*H, 2, kSelCandMax, 2]: the k-th bin's (key, index) per round
   uint32_t* health;      // health words (call's, sticky) or nullptr
   int zero_sync;         // 1: clear the sync words first (0: the score call just did)
 };

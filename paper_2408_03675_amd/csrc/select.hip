@@ -18,29 +18,11 @@
 // head's counter, wait for the other slices), and every work-group takes the
 // same decisions from the same published data.
 //
-// Sliced heads:
-// Top-k of one key set (k-th largest key T, and `need`, how many keys equal
-// to T belong to the top k; ties go to the lowest indices):
-//   1. pivots: the keys of about kSelSamples sampled tokens (every st-th
-//      token of the head) give a window [lo, hi] that holds the k-th largest
-//      key with high probability (ranks k*m/n -+ a few standard deviations);
-//   2. one counting pass: keys above the window and inside it, per slice;
-//      each slice also publishes its keys inside the window with their
-//      indices (the window is narrow, typically about 1500 tokens);
-//   3. if the window holds the k-th key and all its keys were published, an
-//      exact radix select over them in LDS gives T and need; a window of one
-//      value gives them from the counts; otherwise the window is halved in
-//      key space and counted again (a fallback for degenerate pivots).
-// The top k is then "key > T, or key == T with a rank among the T-keys,
-// in index order, below need": a block scan gives each slice its ranks, and
-// every slice knows how many T-keys the slices before it hold.
-//
-// Assembly: every work-group knows, from the published counts, how many
-// tokens each slice keeps, so it writes its kept indices at the right offset
-// of the ascending keep list without another round.
+// (Both kernels are described with their code below.)
 
 #include <type_traits>
 
+#include "../../include/nacl.h"
 #include "device_common.h"
 #include "internal.h"
 #include "gumbel.h"
@@ -308,10 +290,10 @@ __device__ __forceinline__ void wave_sort_desc(uint32_t (&v)[R]) {
 // pieces of four bins in the order (q + l) mod 16, so that the eight lanes
 // an LDS cycle serves touch distinct banks.  Ends with a barrier.
 template <int NRK>
-__device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) {
+__device__ __forceinline__ void pick_bins(uint32_t* hist, uint32_t (*pick)[4], const uint32_t (&kr)[NRK]) {
   if (threadIdx.x < kWave) {
     const int lane = threadIdx.x;
-    uint4* own = reinterpret_cast<uint4*>(s.hist + kHistBins - 64 * (lane + 1));
+    uint4* own = reinterpret_cast<uint4*>(hist + kHistBins - 64 * (lane + 1));
     uint32_t sum = 0u;
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
@@ -324,26 +306,31 @@ __device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) 
     for (int r = 0; r < NRK; ++r) {
       const uint32_t want = kr[r];
       if (want == 0u || want > total) {
-        if (lane == 0) s.pick[r][0] = 0u;
+        if (lane == 0) pick[r][0] = 0u;
         continue;
       }
       const int l0 = (int)__builtin_ctzll(__ballot(incl >= want));
       const uint32_t above = (uint32_t)__builtin_amdgcn_readlane((int)(incl - sum), l0);
       const int b = kHistBins - 1 - 64 * l0 - lane;  // lane m: the m-th bin of lane l0 from the top
-      const uint32_t c = s.hist[b];
+      const uint32_t c = hist[b];
       const uint32_t inc2 = above + wave_inclusive_scan(c);
       const int m = (int)__builtin_ctzll(__ballot(inc2 >= want));
       if (lane == m) {
-        s.pick[r][0] = 1u;
-        s.pick[r][1] = (uint32_t)b;
-        s.pick[r][2] = want - (inc2 - c);
-        s.pick[r][3] = c;
+        pick[r][0] = 1u;
+        pick[r][1] = (uint32_t)b;
+        pick[r][2] = want - (inc2 - c);
+        pick[r][3] = c;
       }
     }
 #pragma unroll
     for (int q = 0; q < 16; ++q) lds_zero16(reinterpret_cast<uint32_t*>(own + ((q + lane) & 15)));
   }
   lds_barrier();
+}
+
+template <int NRK>
+__device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) {
+  pick_bins(s.hist, s.pick, kr);
 }
 
 // The kr-th largest of the keys whose bits at and above `bits` equal those
@@ -619,103 +606,62 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
 
 // ===========================================================================
 // Longer heads: slices of kSelSlice tokens, one work-group each.
+//
+// Thread t of slice p holds the scores and Gumbel keys of the kSelPer
+// consecutive tokens p * kSelSlice + kSelPer * t + i in registers.  The
+// work-groups of a head take the same decisions from the same data: each
+// derives the window from the same sampled tokens (read from memory), and
+// they exchange histograms and candidate lists through the workspace in
+// rounds (publish with device-coherent stores, count an arrival on the
+// head's counter, wait for the other slices).  Top-k of one key set:
+//   1. window: 1024 tokens spread evenly over the head are sampled (Pi and
+//      tokens already taken left out); the bins of their top 12 bits that
+//      hold the sample ranks k*m/n -/+ three standard deviations give
+//      [lo, hi);
+//   2. each slice counts its keys in [lo, top) in 4095 equal bins of width
+//      2^sh over [lo, hi) plus one bin for the rest (top is unbounded in the
+//      first pass), and publishes the bins and their totals per group of
+//      64; after the round every work-group reads the group totals of all
+//      slices, then the bins of the group holding the k-th key, and so the
+//      bin holding it and how many keys each slice has above it and in it;
+//   3. if that bin is one key value wide, or the top k takes all of it, the
+//      threshold follows from the counts; if it holds at most kSelCandMax
+//      keys, the slices publish them (key, index) in index order and every
+//      work-group ranks them; otherwise, or if the window missed the k-th
+//      key, the window moves to that bin (or below lo, or above the regular
+//      bins) and step 2 repeats.
+// The top k is then "key > T, or key == T with a rank among the T-keys, in
+// index order, below need"; every work-group knows each slice's count of
+// taken keys, so the assembly writes each slice's kept indices at their
+// offset of the keep list without another round.
 
-// Exclusive prefix of v over the work-group in thread order, and the total.
-__device__ uint32_t block_scan_total(uint32_t v, uint32_t* scan_buf, uint32_t& total) {
-  const uint32_t ex = block_exclusive_scan(v, scan_buf);
-  total = scan_buf[2 * kSelWaves - 1];
-  __syncthreads();  // every thread has read the total before the buffer is reused
-  return ex;
-}
+constexpr int kSliceHistWords = kHistBins + kHistBins / kWave;  // bins, then the 64 group totals
+static_assert(kSliceHistWords == kSelHistWords, "published histogram size");
+constexpr int kSelMaxPasses = 16;
 
-struct SelLds {
-  uint32_t a[kSelCapTotal];     // sampled keys, then window keys
-  uint32_t b[kSelCapTotal];     // window token indices
-  uint32_t smp[2][kSelSamples]; // sampled keys of a head held by one slice
-  uint32_t hist[256];
+struct SliceLds {
+  alignas(16) uint32_t hist[kHistBins];  // all zero between passes
+  uint32_t ppos[NACL_MAX_P];             // protected positions, ascending
+  uint32_t ckey[kSelCandMax], cidx[kSelCandMax];
+  uint32_t above[kSelMaxSlices];  // per slice: keys above the current window (this selection)
+  uint32_t inbin[kSelMaxSlices];  // per slice: keys in the k-th bin
+  uint32_t gt[kSelMaxSlices];     // per slice: keys of the k-th bin above T
+  uint32_t eq[kSelMaxSlices];     // per slice: keys equal to T
+  uint32_t taken[2][kSelMaxSlices];
+  uint32_t prot[kSelMaxSlices];
+  uint32_t pick[2][4];
   uint32_t scan[2 * kSelWaves];
   uint32_t shv[16];
-  uint32_t cnt_gt[kSelMaxSlices];   // per slice: keys above the window (this round)
-  uint32_t cnt_in[kSelMaxSlices];   // per slice: keys inside the window
-  uint32_t off_in[kSelMaxSlices];   // prefix of cnt_in
-  uint32_t gt_t[kSelMaxSlices];     // per slice: keys above T
-  uint32_t ties[kSelMaxSlices];     // per slice: keys equal to T
-  uint32_t taken[2][kSelMaxSlices]; // per slice: tokens of u_score / u_random
-  uint32_t prot[kSelMaxSlices];     // per slice: protected proxies
 };
 
-// hist[bin] += 1 for every lane with `valid`.  The keys cluster (scores
-// share a few exponents) and same-address atomics of one instruction are
-// serialised, so the most common bins of the wave are counted first with one
-// atomic each (up to three of them, the bins of the first pending lanes); the
-// lanes left over add one each.
-__device__ __forceinline__ void wave_count(uint32_t* hist, uint32_t bin, bool valid) {
-  const int lane = threadIdx.x & 63;
-  uint64_t todo = __ballot(valid);
-#pragma unroll
-  for (int r = 0; r < 3; ++r) {
-    if (!todo) return;
-    const int leader = __builtin_ctzll(todo);
-    const uint32_t b0 = __builtin_amdgcn_readlane(bin, leader);
-    const uint64_t m = __ballot(valid && bin == b0) & todo;
-    if (lane == leader) atomicAdd(&hist[b0], (uint32_t)__popcll(m));
-    todo &= ~m;
-  }
-  if ((todo >> lane) & 1u) atomicAdd(&hist[bin], 1u);
-}
-
-// The k-th largest (1 <= k <= n) of the n keys in s.a, by four 8-bit radix
-// passes over LDS; returns T and sets need = how many keys equal to T the
-// top k holds.
-__device__ uint32_t lds_kth(SelLds& s, int n, uint32_t k, uint32_t& need) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  uint32_t prefix = 0u, pmask = 0u, kr = k;
-#pragma unroll 1
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (tid < 256) s.hist[tid] = 0u;
-    __syncthreads();
-    for (int i0 = 0; i0 < n; i0 += kSelThreads) {
-      const int i = i0 + tid;
-      const uint32_t v = i < n ? s.a[i] : 0u;
-      wave_count(s.hist, (v >> shift) & 255u, i < n && (v & pmask) == prefix);
-    }
-    __syncthreads();
-    if (wave == 0) {
-      // lane l holds bins 255 - 4l down to 252 - 4l (descending key order)
-      uint32_t c[4], sum = 0u;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        c[q] = s.hist[255 - 4 * lane - q];
-        sum += c[q];
-      }
-      const uint32_t incl = wave_inclusive_scan(sum);
-      const uint32_t excl = incl - sum;
-      if (excl < kr && kr <= incl) {
-        uint32_t cum = excl;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (cum < kr && kr <= cum + c[q]) {
-            s.shv[0] = (uint32_t)(255 - 4 * lane - q);
-            s.shv[1] = kr - cum;
-          }
-          cum += c[q];
-        }
-      }
-    }
-    __syncthreads();
-    prefix |= s.shv[0] << shift;
-    pmask |= 255u << shift;
-    kr = s.shv[1];
-    __syncthreads();
-  }
-  need = kr;
-  return prefix;
+// Sum over the wave.
+__device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)wave_inclusive_scan(x), kWave - 1);
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
-  __shared__ SelLds s;
-  const int tid = threadIdx.x;
+  __shared__ SliceLds s;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = a.L, nb = a.nb;
   if (tid == 0) s.shv[0] = atomicAdd(a.sync, 1u);
   __syncthreads();
@@ -728,40 +674,36 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
     return;
   }
   const int bh = ticket / nb, part = ticket % nb;
-  const int b = bh / a.H, h = bh % a.H;
-  const int st = select_sample_stride(L);
-  const int m_all = (L + st - 1) / st;                 // sampled tokens of the head
   uint32_t* counter = a.sync + 64 + bh;
-  uint32_t* samples = a.samples + (int64_t)bh * 2 * a.ms;
-  const int j0 = part * kSelSlice + tid * kSelPer;    // this thread's first token
-  const int nrem = L - j0;                             // tokens of the head from j0 on
+  const int j0 = part * kSelSlice + tid * kSelPer;  // this thread's first token
+  const int nrem = L - j0;                          // tokens of the head from j0 on
   const int pbase = a.P - a.n_protect;
+  const uint32_t* frow = reinterpret_cast<const uint32_t*>(a.scores) + (int64_t)bh * L;
+  const uint32_t* grow = a.keys2 + (int64_t)bh * L;
   int round = 0;
+  bool gave_up = false;  // a wait or the pass limit gave up (never expected)
 
   // Arrival on the head's counter, then wait for every slice of the head.
   auto exchange = [&]() {
     wait_stores();
     __syncthreads();
-    if (tid == 0 && nb > 1) {
+    if (tid == 0) {
       atomicAdd(counter, 1u);
       const uint32_t target = (uint32_t)nb * (uint32_t)(round + 1);
       uint32_t spins = 0;
       while (load_coherent(counter) < target) {
         __builtin_amdgcn_s_sleep(1);
         if (++spins > kSelSpinLimit) {
-          if (a.health) {
-            atomicOr(a.health, 8u);
-            atomicOr(a.health + 1, 8u);
-          }
+          s.shv[9] = 1u;
           break;
         }
       }
     }
     ++round;
     __syncthreads();
+    gave_up = gave_up || s.shv[9] != 0u;
   };
 
-  // ---- this thread's tokens: scores, Gumbel keys, protected marks
   // This thread's kSelPer consecutive tokens of a row (16-byte loads when
   // the row allows; past the end of the head the last token repeats and is
   // masked below).
@@ -780,26 +722,32 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
       for (int i = 0; i < kSelPer; ++i) out[i] = row[nrem > 0 ? j0 + min(i, nrem - 1) : L - 1];
     }
   };
-  uint32_t fk[kSelPer];
-  const uint32_t* gsrc = a.keys2 + (int64_t)bh * L;
-  load_row(reinterpret_cast<const uint32_t*>(a.scores) + (int64_t)bh * L, fk);
-  // The protected positions (ascending, at most NACL_MAX_P) staged in LDS.
+  uint32_t fk[kSelPer], gk[kSelPer];
+  load_row(frow, fk);
+  if (a.Cr > 0) load_row(grow, gk);
+
+  // The protected positions staged in LDS.
   const int np = a.n_protect;
-  uint32_t* ppos = s.b;
-  for (int i = tid; i < np; i += kSelThreads) ppos[i] = (uint32_t)a.pos[pbase + i];
+  for (int i = tid; i < np; i += kSelThreads) s.ppos[i] = (uint32_t)a.pos[pbase + i];
+  if (tid >= 1 && tid < 16) s.shv[tid] = 0u;  // shv[0] (the ticket) is next written after barriers
+  for (int i = tid; i < kHistBins; i += kSelThreads) s.hist[i] = 0u;
   __syncthreads();
   auto first_at_least = [&](int x) {  // first staged position >= x
     int lo = 0, hi = np;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
-      if ((int)ppos[mid] < x) lo = mid + 1;
+      if ((int)s.ppos[mid] < x) lo = mid + 1;
       else hi = mid;
     }
     return lo;
   };
+  auto protected_token = [&](int j) {
+    const int i = first_at_least(j);
+    return i < np && (int)s.ppos[i] == j;
+  };
   uint32_t prot = 0u;  // bit i: token j0 + i is protected
   if (np > 0 && j0 < L)
-    for (int i = first_at_least(j0); i < np && (int)ppos[i] < j0 + kSelPer; ++i) prot |= 1u << (ppos[i] - j0);
+    for (int i = first_at_least(j0); i < np && (int)s.ppos[i] < j0 + kSelPer; ++i) prot |= 1u << (s.ppos[i] - j0);
 #pragma unroll
   for (int i = 0; i < kSelPer; ++i) {
     const bool cand = i < nrem && !((prot >> i) & 1u);
@@ -807,289 +755,287 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
   }
   // Protected proxies per slice (for the assembly offsets).
   if (tid < nb) s.prot[tid] = (uint32_t)(first_at_least((tid + 1) * kSelSlice) - first_at_least(tid * kSelSlice));
-  __syncthreads();  // the staged positions are dead from here on
 
-  // ---- round 0: sampled (score key, Gumbel key) pairs
-  {
-    int nxt = (j0 + st - 1) / st * st, slot = nxt / st;  // first sampled token >= j0
-    int di = nxt - j0;                                    // its offset in this thread's run
+  // Top k (1 <= k <= the head's nonzero keys, n_valid of them) of the key
+  // sets key[] of the head's slices; sample(j) is the key of token j (0: not a
+  // candidate).  Sets s.taken[which][q] for every slice; returns this
+  // thread's member mask.
+  auto top_k = [&](const uint32_t (&key)[kSelPer], uint32_t k, uint32_t n_valid, int which, auto&& sample,
+                   uint32_t& T_out) -> uint32_t {
+    // 1. The window from the sample.
+    const uint32_t sk = sample((int)(((int64_t)tid * L) >> 10));
+    if (tid < nb) s.above[tid] = 0u;
+    const uint64_t sb = __ballot(sk != 0u);
+    if (lane == 0 && sb) atomicAdd(&s.shv[6], (uint32_t)__popcll(sb));
+    if (sk != 0u) atomicAdd(&s.hist[sk >> 20], 1u);
+    __syncthreads();
+    const uint32_t n_s = s.shv[6];
+    const float e = (float)k * (float)n_s / (float)n_valid;
+    const float dev = 3.f * sqrtf(e) + 3.f;
+    const uint32_t want[2] = {n_s ? min(n_s, (uint32_t)ceilf(e + dev)) : 0u,
+                              n_s ? (e - dev >= 1.f ? (uint32_t)(e - dev) : 1u) : 0u};
+    pick_bins(s.hist, s.pick, want);
+    uint32_t lo = 1u;
+    uint64_t hi = 1ull << 32;
+    if (s.pick[0][0] != 0u) {
+      lo = max(1u, s.pick[0][1] << 20);
+      hi = (uint64_t)(s.pick[1][1] + 1u) << 20;  // rank 1 always exists when rank want[0] does
+    }
+    __syncthreads();  // pick and sample count read
+    if (tid == 0) s.shv[6] = 0u;
+
+    // 2-3. Passes over [lo, top) until the k-th key's bin is resolved.
+    bool open = true;  // top unbounded: bin 4095 takes every key past the regular bins
+    uint32_t krem = k, T = 0u, need = 0u;
+    bool all_bin = false;
+#pragma unroll 1
+    for (int pass = 0;; ++pass) {
+      const uint64_t range = hi > (uint64_t)lo ? hi - lo : 1u;
+      int sh = 0;
+      while (((uint64_t)(kHistBins - 1) << sh) < range) ++sh;
 #pragma unroll
-    for (int i = 0; i < kSelPer; ++i)
-      if (i == di && i < nrem) {
-        const uint32_t g = a.Cr > 0 && fk[i] != 0u ? gsrc[nxt] : 0u;
-        if (nb == 1) {  // one slice: the sample stays in LDS
-          s.smp[0][slot] = fk[i];
-          s.smp[1][slot] = g;
+      for (int i = 0; i < kSelPer; ++i)
+        if (key[i] >= lo && (open || (uint64_t)key[i] < hi))
+          atomicAdd(&s.hist[min((key[i] - lo) >> sh, (uint32_t)(kHistBins - 1))], 1u);
+      __syncthreads();
+      // Publish the bins (thread t: bins 4t .. 4t + 3, then clears them) and
+      // the group totals (group g: bins 4095 - 64 g down to 4032 - 64 g, the
+      // bins of the 16 threads of one 16-lane row).
+      {
+        uint32_t* xh = a.xhist + (((int64_t)bh * 2 + (round & 1)) * nb + part) * kSliceHistWords;
+        uint32_t c4 = 0u;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t v = s.hist[4 * tid + u];
+          store_coherent(xh + 4 * tid + u, v);
+          s.hist[4 * tid + u] = 0u;
+          c4 += v;
+        }
+        uint32_t r = c4;
+        r += dpp_or_zero<0x111, 0xf>(r);
+        r += dpp_or_zero<0x112, 0xf>(r);
+        r += dpp_or_zero<0x114, 0xf>(r);
+        r += dpp_or_zero<0x118, 0xf>(r);
+        if ((tid & 15) == 15) store_coherent(xh + kHistBins + (kWave - 1 - (tid >> 4)), r);
+      }
+      exchange();
+      if (wave == 0) {
+        const uint32_t* base = a.xhist + ((int64_t)bh * 2 + ((round - 1) & 1)) * nb * kSliceHistWords;
+        uint32_t gsum = 0u;
+        for (int q = 0; q < nb; ++q) gsum += load_coherent(base + q * kSliceHistWords + kHistBins + lane);
+        const uint32_t incl = wave_inclusive_scan(gsum);
+        const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
+        if (total < krem) {
+          // Every key at or above lo is taken; the k-th key lies below lo.
+          for (int q = 0; q < nb; ++q) {
+            const uint32_t tq = wave_sum(load_coherent(base + q * kSliceHistWords + kHistBins + lane));
+            if (lane == 0) s.above[q] += tq;
+          }
+          if (lane == 0) {
+            s.shv[0] = 1u;
+            s.shv[1] = total;
+          }
         } else {
-          store_coherent(samples + slot, fk[i]);
-          store_coherent(samples + a.ms + slot, g);
-        }
-        nxt += st;
-        di += st;
-        ++slot;
-      }
-  }
-  if (nb == 1) __syncthreads();
-  else exchange();
-
-  uint32_t sel[2] = {0u, 0u};  // bit i: token j0 + i in u_score / u_random
-  // Top-k of key[] (this thread's tokens; 0 = not a candidate) among n
-  // candidates of the head; `which` indexes taken[].  samp(x) maps a sampled
-  // pair index to its key for this selection (0 = not a candidate).
-  auto top_k = [&](const uint32_t (&key)[kSelPer], uint32_t k, uint32_t n, int which, uint32_t& T_out,
-                   auto&& samp) -> uint32_t {
-    // Pivots: wave 0 sorts the sampled keys (zero past the sample and for
-    // tokens that are not candidates) in registers.
-    if (tid < kWave) {
-      constexpr int R = kSelSamples / kWave;
-      uint32_t sv[R];
-#pragma unroll
-      for (int r = 0; r < R; ++r) {
-        const int x = tid * R + r;
-        sv[r] = x < m_all ? samp(x) : 0u;
-      }
-      uint32_t nz = 0;
-#pragma unroll
-      for (int r = 0; r < R; ++r) nz += sv[r] != 0u;
-      wave_sort_desc(sv);
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) nz += (uint32_t)__shfl_xor((int)nz, off);
-#pragma unroll
-      for (int r = 0; r < R; ++r) s.a[tid * R + r] = sv[r];
-      if (tid == 0) s.shv[13] = nz;
-    }
-    __syncthreads();
-    const uint32_t m = s.shv[13];
-    uint32_t plo = 1u, phi = 0xFFFFFFFFu;
-    if (m > 0) {
-      // rank of the k-th key among the sampled candidates, give or take
-      // three standard deviations, within what the exact step can take
-      const double r = (double)k * (double)m / (double)n;
-      const double sd = sqrt(r * (1.0 - r / (double)m) + 1.0);
-      const double per = (double)n / (double)m;  // candidates per sampled one
-      const int delta = (int)fmin(ceil(3.0 * sd) + 2.0, fmax(1.0, floor(0.45 * kSelCapTotal / per)));
-      const long hr = (long)floor(r) - delta, lr = (long)ceil(r) + delta;
-      if (hr >= 1) phi = s.a[hr - 1];
-      if (lr <= (long)m) plo = s.a[lr - 1];
-    }
-    __syncthreads();
-    // Window search: T lies in [lo, hi], `above` keys lie above hi.
-    uint32_t lo = 1u, hi = 0xFFFFFFFFu, above = 0u, T = 0u, need = 0u;
-    bool done = false;
-    for (int it = 0; !done; ++it) {
-      const int parity = round & 1;
-      uint32_t* rc = a.rounds + ((int64_t)bh * 2 + parity) * nb * 2;
-      uint32_t* mid = a.mid + (((int64_t)bh * 2 + parity) * nb + part) * a.cap_b * 2;
-      // One scan of both counts packed in 16-bit halves (a slice holds at
-      // most kSelSlice = 2^15 tokens).
-      uint32_t gt = 0, in = 0;
-#pragma unroll
-      for (int i = 0; i < kSelPer; ++i) {
-        gt += key[i] > phi;
-        in += key[i] >= plo && key[i] <= phi;
-      }
-      uint32_t tot;
-      const uint32_t ex = block_scan_total(gt | (in << 16), s.scan, tot);
-      const uint32_t gt_tot = tot & 0xFFFFu, in_tot = tot >> 16;
-      uint32_t w = ex >> 16;
-      if (nb == 1) {
-        // One slice: the window's keys go straight to LDS.
-        if (in_tot <= (uint32_t)kSelCapTotal) {
-#pragma unroll
-          for (int i = 0; i < kSelPer; ++i)
-            if (key[i] >= plo && key[i] <= phi) {
-              s.a[w] = key[i];
-              s.b[w] = (uint32_t)(j0 + i);
-              ++w;
+          const int g0 = (int)__builtin_ctzll(__ballot(incl >= krem));
+          const uint32_t above_g = (uint32_t)__builtin_amdgcn_readlane((int)(incl - gsum), g0);
+          const int b = kHistBins - 1 - kWave * g0 - lane;  // lane m: the m-th bin of group g0 from the top
+          uint32_t csum = 0u;
+          for (int q = 0; q < nb; ++q) csum += load_coherent(base + q * kSliceHistWords + b);
+          const uint32_t inc2 = above_g + wave_inclusive_scan(csum);
+          const int m = (int)__builtin_ctzll(__ballot(inc2 >= krem));
+          for (int q = 0; q < nb; ++q) {
+            const uint32_t tg = load_coherent(base + q * kSliceHistWords + kHistBins + lane);
+            const uint32_t cb = load_coherent(base + q * kSliceHistWords + b);
+            const uint32_t ab = wave_sum((lane < g0 ? tg : 0u) + (lane < m ? cb : 0u));
+            const uint32_t ib = (uint32_t)__builtin_amdgcn_readlane((int)cb, m);
+            if (lane == 0) {
+              s.above[q] += ab;
+              s.inbin[q] = ib;
             }
+          }
+          const uint32_t cm = (uint32_t)__builtin_amdgcn_readlane((int)csum, m);
+          const uint32_t im = (uint32_t)__builtin_amdgcn_readlane((int)inc2, m);
+          if (lane == 0) {
+            s.shv[0] = 0u;
+            s.shv[1] = (uint32_t)(kHistBins - 1 - kWave * g0 - m);
+            s.shv[2] = krem - (im - cm);
+            s.shv[3] = cm;
+          }
         }
-        if (tid == 0) {
-          s.cnt_gt[0] = gt_tot;
-          s.cnt_in[0] = in_tot;
+      }
+      __syncthreads();
+      const uint32_t state = s.shv[0], b1 = s.shv[1], kr = s.shv[2], n1 = s.shv[3];
+      __syncthreads();  // read before the next pass rewrites them
+      if (pass + 1 >= kSelMaxPasses || gave_up) {  // never expected: give up with a valid-looking answer
+        gave_up = true;
+        T = lo;
+        need = 0u;
+        all_bin = true;
+        if (tid < nb) s.inbin[tid] = 0u;
+        break;
+      }
+      if (state == 1) {  // below the window
+        krem -= b1;
+        hi = lo;
+        lo = 1u;
+        open = false;
+        continue;
+      }
+      const uint64_t blo = (uint64_t)lo + ((uint64_t)b1 << sh);
+      if (open && b1 == (uint32_t)(kHistBins - 1)) {  // past the regular bins
+        lo = (uint32_t)blo;
+        hi = 1ull << 32;
+        continue;
+      }
+      if (sh == 0) {  // one key value: T, and how many of its keys to take
+        T = (uint32_t)blo;
+        need = kr;
+        if (tid < nb) {
+          s.gt[tid] = 0u;
+          s.eq[tid] = s.inbin[tid];
         }
-      } else {
-        if (in_tot <= (uint32_t)a.cap_b) {
+        break;
+      }
+      if (kr == n1) {  // the whole bin is taken
+        T = (uint32_t)blo;
+        all_bin = true;
+        break;
+      }
+      if (n1 <= (uint32_t)kSelCandMax) {
+        // The bin's keys, in index order, from every slice.
+        const uint32_t bhi1 = (uint32_t)(blo + ((1ull << sh) - 1u));  // last key value of the bin
+        uint32_t off = 0u;
+        for (int q = 0; q < part; ++q) off += s.inbin[q];
+        uint32_t cnt = 0u;
 #pragma unroll
-          for (int i = 0; i < kSelPer; ++i)
-            if (key[i] >= plo && key[i] <= phi) {
-              store_coherent(mid + 2 * w, key[i]);
-              store_coherent(mid + 2 * w + 1, (uint32_t)(j0 + i));
-              ++w;
+        for (int i = 0; i < kSelPer; ++i) cnt += key[i] >= (uint32_t)blo && key[i] <= bhi1;
+        uint32_t w = off + block_exclusive_scan(cnt, s.scan);
+        uint32_t* xc = a.xcand + ((int64_t)bh * 2 + (round & 1)) * kSelCandMax * 2;
+#pragma unroll
+        for (int i = 0; i < kSelPer; ++i)
+          if (key[i] >= (uint32_t)blo && key[i] <= bhi1) {
+            if (w < (uint32_t)kSelCandMax) {
+              store_coherent(xc + 2 * w, key[i]);
+              store_coherent(xc + 2 * w + 1, (uint32_t)(j0 + i));
             }
-        }
-        if (tid == 0) {
-          store_coherent(rc + 2 * part, gt_tot);
-          store_coherent(rc + 2 * part + 1, in_tot);
+            ++w;
+          }
+        if (tid < nb) {
+          s.gt[tid] = 0u;
+          s.eq[tid] = 0u;
         }
         exchange();
-        if (tid < nb) {
-          s.cnt_gt[tid] = load_coherent(rc + 2 * tid);
-          s.cnt_in[tid] = load_coherent(rc + 2 * tid + 1);
-        }
-      }
-      __syncthreads();
-      if (tid == 0) {
-        uint32_t G = 0, I = 0, full = 1, off = 0;
-        for (int q = 0; q < nb; ++q) {
-          G += s.cnt_gt[q];
-          I += s.cnt_in[q];
-          full &= s.cnt_in[q] <= (uint32_t)(nb == 1 ? kSelCapTotal : a.cap_b);
-          s.off_in[q] = off;
-          off += s.cnt_in[q];
-        }
-        // state: 0 continue, 1 resolved by one value, 2 resolve from the window's keys
-        uint32_t state = 0;
-        if (k <= G) {
-          lo = phi + 1u;
-        } else if (k > G + I) {
-          hi = plo - 1u;
-          above = G + I;
-        } else {
-          lo = plo;
-          hi = phi;
-          above = G;
-          if (plo == phi) state = 1;
-          else if (full && I <= (uint32_t)kSelCapTotal) state = 2;
-        }
-        if (state == 0 && it + 1 >= kSelMaxRounds) {
-          if (a.health) {
-            atomicOr(a.health, 8u);
-            atomicOr(a.health + 1, 8u);
-          }
-          state = 1;  // give up: take the window's low end (never expected)
-          plo = phi = lo;
-        }
-        s.shv[2] = state;
-        s.shv[3] = G;
-        s.shv[4] = I;
-        s.shv[5] = lo;
-        s.shv[6] = hi;
-        s.shv[7] = above;
-        s.shv[8] = plo;
-        s.shv[9] = phi;
-      }
-      __syncthreads();
-      const uint32_t state = s.shv[2], G = s.shv[3], I = s.shv[4];
-      lo = s.shv[5];
-      hi = s.shv[6];
-      above = s.shv[7];
-      if (state == 1) {
-        T = s.shv[8];
-        need = k - G;
-        if (tid < nb) {
-          s.gt_t[tid] = s.cnt_gt[tid];
-          s.ties[tid] = s.cnt_in[tid];
-        }
-        done = true;
-      } else if (state == 2) {
-        // Every slice's window keys into LDS, then the exact step.
-        // (four entries per thread in flight at a time; one slice wrote
-        // them to LDS already)
-        for (int e0 = 0; nb > 1 && e0 < (int)I; e0 += 4 * kSelThreads) {
-          constexpr int kU = 4;
-          uint32_t ka[kU], kb[kU];
-#pragma unroll
-          for (int u = 0; u < kU; ++u) {
-            const int e = e0 + tid + u * kSelThreads;
-            ka[u] = kb[u] = 0u;
-            if (e < (int)I) {
-              int q = 0;
-              while (q + 1 < nb && s.off_in[q + 1] <= (uint32_t)e) ++q;
-              const uint32_t* src = a.mid + (((int64_t)bh * 2 + parity) * nb + q) * a.cap_b * 2 +
-                                    2 * (e - (int)s.off_in[q]);
-              ka[u] = load_coherent(src);
-              kb[u] = load_coherent(src + 1);
-            }
-          }
-#pragma unroll
-          for (int u = 0; u < kU; ++u) {
-            const int e = e0 + tid + u * kSelThreads;
-            if (e < (int)I) {
-              s.a[e] = ka[u];
-              s.b[e] = kb[u];
-            }
-          }
-        }
-        if (tid < nb) {
-          s.gt_t[tid] = s.cnt_gt[tid];
-          s.ties[tid] = 0u;
+        const uint32_t* xr = a.xcand + ((int64_t)bh * 2 + ((round - 1) & 1)) * kSelCandMax * 2;
+        if (tid < (int)n1) {
+          s.ckey[tid] = load_coherent(xr + 2 * tid);
+          s.cidx[tid] = load_coherent(xr + 2 * tid + 1);
         }
         __syncthreads();
-        T = lds_kth(s, (int)I, k - G, need);
-        for (int e0 = 0; e0 < (int)I; e0 += kSelThreads) {
-          const int e = e0 + tid;
-          const uint32_t v = e < (int)I ? s.a[e] : 0u;
-          const uint32_t q = e < (int)I ? s.b[e] / (uint32_t)kSelSlice : 0u;
-          wave_count(s.gt_t, q, e < (int)I && v > T);
-          wave_count(s.ties, q, e < (int)I && v == T);
+        // Candidate t counts the candidates above and equal to its key;
+        // those whose key is the kr-th largest publish it.
+        uint32_t v = 0u, c_gt = 0u, c_eq = 0u;
+        if (tid < (int)n1) {
+          v = s.ckey[tid];
+          for (int j = 0; j < (int)n1; ++j) {
+            const uint32_t c = s.ckey[j];
+            c_gt += c > v ? 1u : 0u;
+            c_eq += c == v ? 1u : 0u;
+          }
+          if (c_gt < kr && kr <= c_gt + c_eq) {
+            s.shv[4] = v;
+            s.shv[5] = kr - c_gt;
+          }
         }
-        done = true;
-      } else {
-        // Halve the window in key space: count [mid, hi] next.
-        plo = lo + ((hi - lo) >> 1) + (hi > lo ? 1u : 0u);
-        phi = hi;
+        __syncthreads();
+        T = s.shv[4];
+        need = s.shv[5];
+        if (tid < (int)n1) {
+          const uint32_t q = s.cidx[tid] / (uint32_t)kSelSlice;
+          if (v > T) atomicAdd(&s.gt[q], 1u);
+          if (v == T) atomicAdd(&s.eq[q], 1u);
+        }
+        __syncthreads();
+        break;
       }
-      __syncthreads();
+      // Narrow the window to the bin.
+      lo = (uint32_t)blo;
+      hi = blo + (1ull << sh);
+      open = false;
+      krem = kr;
     }
-      // Tokens each slice takes, and this slice's tie offset.
+    T_out = T;  // the same in every work-group of the head
+    // Each slice's taken keys, and this slice's offset among the T-keys.
     if (tid == 0) {
-      uint32_t toff = 0, mine = 0;
+      uint32_t toff = 0u, mine = 0u;
       for (int q = 0; q < nb; ++q) {
-        const uint32_t tq = s.ties[q];
-        const uint32_t take = need > toff ? min(need - toff, tq) : 0u;
-        s.taken[which][q] = s.gt_t[q] + take;
-        if (q == part) mine = toff;
-        toff += tq;
+        uint32_t t = s.above[q];
+        if (all_bin) {
+          t += s.inbin[q];
+        } else {
+          const uint32_t tq = s.eq[q];
+          t += s.gt[q] + min(need - min(need, toff), tq);
+          if (q == part) mine = toff;
+          toff += tq;
+        }
+        s.taken[which][q] = t;
       }
-      s.shv[10] = mine;
+      s.shv[7] = mine;
     }
     __syncthreads();
-    const uint32_t tie_off = s.shv[10];
-    T_out = T;
-    uint32_t nt = 0;
-#pragma unroll
-    for (int i = 0; i < kSelPer; ++i) nt += key[i] == T;
-    uint32_t tt;
-    uint32_t rank = tie_off + block_scan_total(nt, s.scan, tt);
     uint32_t mask = 0u;
+    if (all_bin) {
 #pragma unroll
-    for (int i = 0; i < kSelPer; ++i) {
-      bool take = key[i] > T;
-      if (key[i] == T) {
-        take = rank < need;
-        ++rank;
+      for (int i = 0; i < kSelPer; ++i) mask |= (key[i] >= T && key[i] != 0u ? 1u : 0u) << i;
+    } else {
+      uint32_t nt = 0u;
+#pragma unroll
+      for (int i = 0; i < kSelPer; ++i) nt += key[i] == T;
+      uint32_t rank = s.shv[7] + block_exclusive_scan(nt, s.scan);
+#pragma unroll
+      for (int i = 0; i < kSelPer; ++i) {
+        bool take = key[i] > T;
+        if (key[i] == T) {
+          take = rank < need;
+          ++rank;
+        }
+        if (take) mask |= 1u << i;
       }
-      if (take) mask |= 1u << i;
     }
+    __syncthreads();  // shv[7] and the scan buffer read before reuse
     return mask;
   };
 
+  uint32_t sel[2] = {0u, 0u};  // bit i: token j0 + i in u_score / u_random
   if (tid < nb) {
     s.taken[0][tid] = 0u;
     s.taken[1][tid] = 0u;
   }
   __syncthreads();
-  const uint32_t n1 = (uint32_t)(L - a.n_protect);
-  uint32_t T1 = 0xFFFFFFFFu, T2 = 0u;
-  if (a.Cp > 0) {
-    sel[0] = top_k(fk, (uint32_t)a.Cp, n1, 0, T1,
-                   [&](int x) { return nb == 1 ? s.smp[0][x] : load_coherent(samples + x); });
-  }
+  auto score_key = [&](int j) -> uint32_t {
+    return protected_token(j) ? 0u : float_order_key(__uint_as_float(frow[j]));
+  };
+  // The score threshold (every work-group of the head has the same), for
+  // leaving u_score out of the draw's sample: tokens whose score key reaches
+  // it count as taken (the sample is only a guess).
+  uint32_t T1 = 0xFFFFFFFFu;
+  if (a.Cp > 0) sel[0] = top_k(fk, (uint32_t)a.Cp, (uint32_t)(L - a.n_protect), 0, score_key, T1);
   if (a.Cr > 0) {
-    // Candidates of the draw: R minus u_score; their Gumbel keys are loaded
-    // only now, when the score keys die.
-    uint32_t gk[kSelPer];
-    load_row(gsrc, gk);
+    // Candidates of the draw: R minus u_score.
 #pragma unroll
     for (int i = 0; i < kSelPer; ++i)
       if (fk[i] == 0u || ((sel[0] >> i) & 1u)) gk[i] = 0u;
-    // Sampled tokens already in u_score are left out of the pivots (ties at
-    // the score threshold counted as taken; the pivots are only a guess).
-    sel[1] = top_k(gk, (uint32_t)a.Cr, n1 - (uint32_t)a.Cp, 1, T2, [&](int x) {
-      const uint32_t f = nb == 1 ? s.smp[0][x] : load_coherent(samples + x);
-      const uint32_t g = nb == 1 ? s.smp[1][x] : load_coherent(samples + a.ms + x);
-      return (f != 0u && f < T1) ? g : 0u;
-    });
+    uint32_t T2;
+    sel[1] = top_k(
+        gk, (uint32_t)a.Cr, (uint32_t)(L - a.n_protect - a.Cp), 1,
+        [&](int j) -> uint32_t {
+          const uint32_t f = score_key(j);
+          return (f != 0u && f < T1) ? grow[j] : 0u;
+        },
+        T2);
+  }
+  if (gave_up && tid == 0 && a.health) {
+    atomicOr(a.health, 8u);
+    atomicOr(a.health + 1, 8u);
   }
 
   // ---- assembly: this slice's kept tokens at their offset of the keep list
@@ -1101,8 +1047,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
     s.shv[12] = base;
   }
   __syncthreads();
-  uint32_t tot;
-  uint32_t o = s.shv[12] + block_scan_total((uint32_t)__popc(kept), s.scan, tot);
+  uint32_t o = s.shv[12] + block_exclusive_scan((uint32_t)__popc(kept), s.scan);
   int32_t* out = a.keep + (int64_t)bh * a.C;
 #pragma unroll
   for (int i = 0; i < kSelPer; ++i)

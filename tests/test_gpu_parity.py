@@ -205,6 +205,42 @@ def test_select_exact_on_identical_scores(case):
             assert np.array_equal(keep[b, h], ref["keep"]), (name, b, h)
 
 
+LONG_SELECT_CASES = [
+    # heads longer than 32768 tokens (one work-group per 16384-token slice):
+    # ties, odd lengths, tiny and near-total budgets, no or only random tokens
+    # name, L, P, n_protect, C, Cr, mode, ties
+    ("long_ties_65k", 65536, 64, 64, 13107, 6553, SAMPLE_SOFTMAX, True),
+    ("odd_40001", 40001, 17, 17, 8000, 3000, SAMPLE_PROPORTIONAL, False),
+    ("small_k_100k", 100000, 128, 128, 300, 100, SAMPLE_SOFTMAX, False),
+    ("large_budget_70k", 70000, 32, 32, 69000, 30000, SAMPLE_SOFTMAX, False),
+    ("uniform_ties_50k", 50000, 64, 32, 10000, 5000, SAMPLE_UNIFORM, True),
+    ("no_random_33k", 32769, 16, 16, 6000, 0, SAMPLE_SOFTMAX, False),
+    ("all_random_45k", 45000, 16, 16, 9000, 8984, SAMPLE_SOFTMAX, False),
+    ("keep_all_36k", 36000, 8, 8, 36000, 10000, SAMPLE_SOFTMAX, False),
+    ("heavy_ties_128k", 131072, 512, 512, 26214, 15728, SAMPLE_SOFTMAX, True),
+]
+
+
+@pytest.mark.parametrize("case", LONG_SELECT_CASES, ids=[c[0] for c in LONG_SELECT_CASES])
+def test_select_exact_long_heads(case):
+    name, L, P, n_protect, C, Cr, mode, ties = case
+    _say("long select case", name)
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    F = rng.gamma(0.3, 1.0 / L, size=(1, 2, L))
+    if ties:
+        F = np.round(F * L * 4) / (L * 4)
+    F32 = F.astype(np.float32)
+    pos = list(range(L - P, L))
+    prob = nacl.Problem(1, 2, L, 128, "bf16", pos, n_protect=n_protect)
+    ws = nacl.workspace(prob)
+    keep = nacl.select(prob, torch.from_numpy(F32).cuda(), C, Cr, mode, seed=1234, layer=5, ws=ws)
+    keep = keep.cpu().numpy()
+    assert nacl.health(ws) == (0, 0)
+    for h in range(2):
+        ref = select_head(F32[0, h], pos, n_protect, C, Cr, mode, 1234, 5, 0, h)
+        assert np.array_equal(keep[0, h], ref["keep"]), (name, h)
+
+
 def test_select_full_length_limit_head():
     """A long head (131072 tokens, the 128k workload's length)."""
     L, P, C, Cr = 131072, 512, 26214, 15728
