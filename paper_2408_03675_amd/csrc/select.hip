@@ -652,7 +652,14 @@ struct SliceLds {
   uint32_t pick[2][4];
   uint32_t scan[2 * kSelWaves];
   uint32_t shv[16];
+  uint32_t list[kSelSlice];       // this slice's kept indices, in order
 };
+
+// store_coherent's 16-byte form: a vector store at the device coherence
+// point (sc1), made complete by wait_stores() like the others.
+__device__ __forceinline__ void store_coherent16(uint32_t* p, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+}
 
 // Sum over the wave.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
@@ -722,9 +729,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
       for (int i = 0; i < kSelPer; ++i) out[i] = row[nrem > 0 ? j0 + min(i, nrem - 1) : L - 1];
     }
   };
-  uint32_t fk[kSelPer], gk[kSelPer];
+  uint32_t fk[kSelPer];
   load_row(frow, fk);
-  if (a.Cr > 0) load_row(grow, gk);
+  // This thread's sampled token, the same in every slice of the head.
+  const int js = (int)(((int64_t)tid * L) >> 10);
+  const uint32_t f_smp = frow[js], g_smp = a.Cr > 0 ? grow[js] : 0u;
 
   // The protected positions staged in LDS.
   const int np = a.n_protect;
@@ -757,13 +766,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
   if (tid < nb) s.prot[tid] = (uint32_t)(first_at_least((tid + 1) * kSelSlice) - first_at_least(tid * kSelSlice));
 
   // Top k (1 <= k <= the head's nonzero keys, n_valid of them) of the key
-  // sets key[] of the head's slices; sample(j) is the key of token j (0: not a
-  // candidate).  Sets s.taken[which][q] for every slice; returns this
-  // thread's member mask.
-  auto top_k = [&](const uint32_t (&key)[kSelPer], uint32_t k, uint32_t n_valid, int which, auto&& sample,
+  // sets key[] of the head's slices; thread t's sampled key is that of token
+  // (t * L) / 1024 (0: not a candidate).  Sets s.taken[which][q] for every
+  // slice; returns this thread's member mask.
+  auto top_k = [&](const uint32_t (&key)[kSelPer], uint32_t k, uint32_t n_valid, int which, uint32_t sk,
                    uint32_t& T_out) -> uint32_t {
-    // 1. The window from the sample.
-    const uint32_t sk = sample((int)(((int64_t)tid * L) >> 10));
+    // 1. The window from the sample (sk: this thread's sampled key).
     if (tid < nb) s.above[tid] = 0u;
     const uint64_t sb = __ballot(sk != 0u);
     if (lane == 0 && sb) atomicAdd(&s.shv[6], (uint32_t)__popcll(sb));
@@ -803,15 +811,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
       // bins of the 16 threads of one 16-lane row).
       {
         uint32_t* xh = a.xhist + (((int64_t)bh * 2 + (round & 1)) * nb + part) * kSliceHistWords;
-        uint32_t c4 = 0u;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const uint32_t v = s.hist[4 * tid + u];
-          store_coherent(xh + 4 * tid + u, v);
-          s.hist[4 * tid + u] = 0u;
-          c4 += v;
-        }
-        uint32_t r = c4;
+        u32x4* mine = reinterpret_cast<u32x4*>(s.hist + 4 * tid);
+        const u32x4 v = *mine;
+        store_coherent16(xh + 4 * tid, v);
+        *mine = u32x4{0u, 0u, 0u, 0u};
+        uint32_t r = v.x + v.y + v.z + v.w;
         r += dpp_or_zero<0x111, 0xf>(r);
         r += dpp_or_zero<0x112, 0xf>(r);
         r += dpp_or_zero<0x114, 0xf>(r);
@@ -820,9 +824,31 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
       }
       exchange();
       if (wave == 0) {
+        // Lane g: group g's totals; then lane m: the m-th bin of the group
+        // holding the k-th key.  The slices' words are loaded eight at a time.
         const uint32_t* base = a.xhist + ((int64_t)bh * 2 + ((round - 1) & 1)) * nb * kSliceHistWords;
+        auto sum_over_slices = [&](int word) {
+          uint32_t sum = 0u;
+          for (int q0 = 0; q0 < nb; q0 += 8) {
+            uint32_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+              v[u] = q0 + u < nb ? load_coherent(base + (q0 + u) * kSliceHistWords + word) : 0u;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) sum += v[u];
+          }
+          return sum;
+        };
+        // Up to eight slices keep their words in registers between the
+        // steps; more slices load them again.
+        uint32_t tg8[8], cb8[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          tg8[u] = u < nb ? load_coherent(base + u * kSliceHistWords + kHistBins + lane) : 0u;
         uint32_t gsum = 0u;
-        for (int q = 0; q < nb; ++q) gsum += load_coherent(base + q * kSliceHistWords + kHistBins + lane);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) gsum += tg8[u];
+        if (nb > 8) gsum = sum_over_slices(kHistBins + lane);
         const uint32_t incl = wave_inclusive_scan(gsum);
         const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
         if (total < krem) {
@@ -839,18 +865,30 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
           const int g0 = (int)__builtin_ctzll(__ballot(incl >= krem));
           const uint32_t above_g = (uint32_t)__builtin_amdgcn_readlane((int)(incl - gsum), g0);
           const int b = kHistBins - 1 - kWave * g0 - lane;  // lane m: the m-th bin of group g0 from the top
+#pragma unroll
+          for (int u = 0; u < 8; ++u) cb8[u] = u < nb ? load_coherent(base + u * kSliceHistWords + b) : 0u;
           uint32_t csum = 0u;
-          for (int q = 0; q < nb; ++q) csum += load_coherent(base + q * kSliceHistWords + b);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) csum += cb8[u];
+          if (nb > 8) csum = sum_over_slices(b);
           const uint32_t inc2 = above_g + wave_inclusive_scan(csum);
           const int m = (int)__builtin_ctzll(__ballot(inc2 >= krem));
-          for (int q = 0; q < nb; ++q) {
-            const uint32_t tg = load_coherent(base + q * kSliceHistWords + kHistBins + lane);
-            const uint32_t cb = load_coherent(base + q * kSliceHistWords + b);
-            const uint32_t ab = wave_sum((lane < g0 ? tg : 0u) + (lane < m ? cb : 0u));
-            const uint32_t ib = (uint32_t)__builtin_amdgcn_readlane((int)cb, m);
-            if (lane == 0) {
-              s.above[q] += ab;
-              s.inbin[q] = ib;
+          for (int q0 = 0; q0 < nb; q0 += 8) {
+            uint32_t tg[8], cb[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const bool ok = q0 + u < nb;
+              tg[u] = q0 == 0 ? tg8[u] : (ok ? load_coherent(base + (q0 + u) * kSliceHistWords + kHistBins + lane) : 0u);
+              cb[u] = q0 == 0 ? cb8[u] : (ok ? load_coherent(base + (q0 + u) * kSliceHistWords + b) : 0u);
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              const uint32_t ab = wave_sum((lane < g0 ? tg[u] : 0u) + (lane < m ? cb[u] : 0u));
+              const uint32_t ib = (uint32_t)__builtin_amdgcn_readlane((int)cb[u], m);
+              if (lane == 0 && q0 + u < nb) {
+                s.above[q0 + u] += ab;
+                s.inbin[q0 + u] = ib;
+              }
             }
           }
           const uint32_t cm = (uint32_t)__builtin_amdgcn_readlane((int)csum, m);
@@ -964,26 +1002,37 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
       krem = kr;
     }
     T_out = T;  // the same in every work-group of the head
-    // Each slice's taken keys, and this slice's offset among the T-keys.
+    // Each slice's taken keys, this slice's offset among the T-keys, and
+    // whether its T-keys are split (some taken, some not).
     if (tid == 0) {
-      uint32_t toff = 0u, mine = 0u;
+      uint32_t toff = 0u, mine = 0u, split = 0u;
       for (int q = 0; q < nb; ++q) {
         uint32_t t = s.above[q];
         if (all_bin) {
           t += s.inbin[q];
         } else {
           const uint32_t tq = s.eq[q];
-          t += s.gt[q] + min(need - min(need, toff), tq);
-          if (q == part) mine = toff;
+          const uint32_t tk = min(need - min(need, toff), tq);
+          t += s.gt[q] + tk;
+          if (q == part) {
+            mine = toff;
+            split = tk != 0u && tk != tq;
+          }
           toff += tq;
         }
         s.taken[which][q] = t;
       }
       s.shv[7] = mine;
+      s.shv[10] = split;
+      s.shv[11] = mine < need;  // this slice's T-keys, if any, are taken when not split
     }
     __syncthreads();
     uint32_t mask = 0u;
-    if (all_bin) {
+    if (!all_bin && s.shv[10] == 0u) {
+      const bool take_t = s.shv[11] != 0u;  // this slice's T-keys: all taken, or none
+#pragma unroll
+      for (int i = 0; i < kSelPer; ++i) mask |= ((take_t ? key[i] >= T : key[i] > T) ? 1u : 0u) << i;
+    } else if (all_bin) {
 #pragma unroll
       for (int i = 0; i < kSelPer; ++i) mask |= (key[i] >= T && key[i] != 0u ? 1u : 0u) << i;
     } else {
@@ -1011,50 +1060,48 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectLaunch a) {
     s.taken[1][tid] = 0u;
   }
   __syncthreads();
-  auto score_key = [&](int j) -> uint32_t {
-    return protected_token(j) ? 0u : float_order_key(__uint_as_float(frow[j]));
-  };
+  const uint32_t fs_key = protected_token(js) ? 0u : float_order_key(__uint_as_float(f_smp));
   // The score threshold (every work-group of the head has the same), for
   // leaving u_score out of the draw's sample: tokens whose score key reaches
   // it count as taken (the sample is only a guess).
   uint32_t T1 = 0xFFFFFFFFu;
-  if (a.Cp > 0) sel[0] = top_k(fk, (uint32_t)a.Cp, (uint32_t)(L - a.n_protect), 0, score_key, T1);
+  if (a.Cp > 0) sel[0] = top_k(fk, (uint32_t)a.Cp, (uint32_t)(L - a.n_protect), 0, fs_key, T1);
   if (a.Cr > 0) {
-    // Candidates of the draw: R minus u_score.
+    // Candidates of the draw: R minus u_score.  (The Gumbel keys are loaded
+    // only now: registers are short while the scores are searched.)
+    uint32_t gk[kSelPer];
+    load_row(grow, gk);
 #pragma unroll
     for (int i = 0; i < kSelPer; ++i)
       if (fk[i] == 0u || ((sel[0] >> i) & 1u)) gk[i] = 0u;
     uint32_t T2;
-    sel[1] = top_k(
-        gk, (uint32_t)a.Cr, (uint32_t)(L - a.n_protect - a.Cp), 1,
-        [&](int j) -> uint32_t {
-          const uint32_t f = score_key(j);
-          return (f != 0u && f < T1) ? grow[j] : 0u;
-        },
-        T2);
+    sel[1] = top_k(gk, (uint32_t)a.Cr, (uint32_t)(L - a.n_protect - a.Cp), 1,
+                   (fs_key != 0u && fs_key < T1) ? g_smp : 0u, T2);
   }
   if (gave_up && tid == 0 && a.health) {
     atomicOr(a.health, 8u);
     atomicOr(a.health + 1, 8u);
   }
 
-  // ---- assembly: this slice's kept tokens at their offset of the keep list
+  // ---- assembly: this slice's kept tokens, listed in LDS, then copied out
+  // with coalesced stores at the slice's offset of the keep list
   uint32_t kept = prot | sel[0] | sel[1];
   if (j0 >= L) kept = 0u;
   if (tid == 0) {
     uint32_t base = 0;
     for (int q = 0; q < part; ++q) base += s.prot[q] + s.taken[0][q] + s.taken[1][q];
     s.shv[12] = base;
+    s.shv[13] = s.prot[part] + s.taken[0][part] + s.taken[1][part];
   }
-  __syncthreads();
-  uint32_t o = s.shv[12] + block_exclusive_scan((uint32_t)__popc(kept), s.scan);
-  int32_t* out = a.keep + (int64_t)bh * a.C;
+  uint32_t o = block_exclusive_scan((uint32_t)__popc(kept), s.scan);
 #pragma unroll
   for (int i = 0; i < kSelPer; ++i)
-    if ((kept >> i) & 1u) {
-      if (o < (uint32_t)a.C) out[o] = j0 + i;
-      ++o;
-    }
+    if ((kept >> i) & 1u) s.list[o++] = (uint32_t)(j0 + i);
+  __syncthreads();
+  const uint32_t base = s.shv[12], n_here = min(s.shv[13], (uint32_t)kSelSlice);
+  int32_t* out = a.keep + (int64_t)bh * a.C;
+  for (uint32_t c = tid; c < n_here; c += kSelThreads)
+    if (base + c < (uint32_t)a.C) out[base + c] = (int32_t)s.list[c];
 }
 
 // Clears the selection's ticket and round counters (a fill kernel rather
