@@ -33,8 +33,8 @@ F32_PEAK_TFLOPS = 157.3        # dense fp32 MFMA
 # (FETCH_SIZE, then WRITE_SIZE) scaled by the same counters on a plain copy of
 # known size; summarised under profiles/.  It is reported only while the
 # kernel source hashes to the value it was measured on.
-MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_split_kernel", "bytes_per_launch": 2209022322,
-                    "source_sha": "b929c07e3b393f98"}
+MEASURED_TRAFFIC = {"workload": "prefill_32k", "kernel": "score_split_kernel", "bytes_per_launch": 2203986978,
+                    "source_sha": "7ab995082e3add45"}
 
 
 def _source_sha(rel):
@@ -107,7 +107,8 @@ def main():
     log(f"[bench] generated {layers} layers in {time.time() - t0:.1f}s")
     q0, k0, v0 = data[0]
     pos_dev = torch.tensor(w.proxy_pos, dtype=torch.int32, device=dev)
-    prob = nacl.Problem.from_tensors(q0, k0, v0, w.proxy_pos, sm_scale=w.scale, proxy_pos_dev=pos_dev)
+    prob = nacl.Problem.from_tensors(q0, k0, v0, w.proxy_pos, n_protect=w.n_protect, sm_scale=w.scale,
+                                     proxy_pos_dev=pos_dev)
     loop = LayerLoop(prob, data, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, streams=args.streams, device=dev)
     n_streams = len(loop.streams)
     ws = loop.workspaces[0]
@@ -364,7 +365,7 @@ def run_configs(oracle_seconds=5.0):
     dev = torch.device("cuda:0")
     nacl.load_library()
     works = [WORKLOADS["small_f32"], WORKLOADS["longbench_4k"]] + sweep_workloads() + \
-        [WORKLOADS["long_128k"], WORKLOADS["prefill_32k"]]
+        [WORKLOADS["long_128k"], WORKLOADS["h2o_4k"], WORKLOADS["prefill_32k"]]
     cache = {}
     for w in works:
         key = (w.B, w.H, w.L, w.D, w.dtype, w.data_seed, w.inject, w.P)
@@ -374,7 +375,8 @@ def run_configs(oracle_seconds=5.0):
             cache[key] = make_layer(w, 0, device=dev)
         q, k, v = cache[key]
         pos_dev = torch.tensor(w.proxy_pos, dtype=torch.int32, device=dev)
-        prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=w.scale, proxy_pos_dev=pos_dev)
+        prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, n_protect=w.n_protect, sm_scale=w.scale,
+                                         proxy_pos_dev=pos_dev)
         ws = nacl.workspace(prob, dev)
         stream = torch.cuda.current_stream(dev)
 

@@ -926,6 +926,13 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
       for (int g0 = 0; g0 < (beyond ? 0 : a.P); g0 += kSplitGroup) {
         const int gn = min(kSplitGroup, a.P - g0);
         load_group(g0, gn);
+        if (pos_g[gn - 1] < chunk_key0) {
+          // No row of the group sees this chunk (rows are sorted by
+          // position): nothing to stream or compute.
+          for (int i = threadIdx.x; i < gn; i += kScoreThreads)
+            store_coherent(part + g0 + i, make_float2(-INFINITY, 0.f));
+          continue;
+        }
         frag_t qf[WB][kS];
         int first, last;
         load_wave_q(gn, qf, first, last);
@@ -1100,9 +1107,11 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
       }
       const float* lse = s.lse_given ? s.lse_in : s.lse2;
       const float lse_mul = s.lse_given ? s.lse_mul : 1.0f;
+      bool fresh = true;  // the item's columns are not yet written
       for (int g0 = 0; g0 < a.P; g0 += kSplitGroup) {
         const int gn = min(kSplitGroup, a.P - g0);
         load_group(g0, gn);
+        if (pos_g[gn - 1] < chunk_key0) continue;  // no row of the group sees this chunk
         frag_t qf[WB][kS];
         int first, last;
         load_wave_q(gn, qf, first, last);
@@ -1157,7 +1166,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
           if (wave == 0) {
             const float z = ((stage[0][lane] + stage[1][lane]) + stage[2][lane]) + stage[3][lane];
             const int idx = t0 * 16 + lane;
-            col_lds[idx] = (g0 == 0 ? 0.f : col_lds[idx]) + z;
+            col_lds[idx] = (fresh ? 0.f : col_lds[idx]) + z;
           }
         };
         k_tiles([&](int t, const frag_t (&kf)[kS], auto u_c) {
@@ -1181,6 +1190,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
         });
         __syncthreads();
         reduce_stage(kSplitTiles - 4);
+        fresh = false;
       }
       __syncthreads();
       float* F = s.scores + (int64_t)bh * a.L;

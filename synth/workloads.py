@@ -26,7 +26,8 @@ class Workload:
     derived with exact rational arithmetic:
         C  = floor(keep_frac * L)
         Cr = floor(random_share * C)
-        n_protect = P (every proxy is kept; Section 5.1)
+        n_protect = P (every proxy is kept; Section 5.1), unless `protect`
+                    says otherwise (0 for the H2O case: every token a proxy)
         Cp = C - n_protect - Cr
     """
     name: str
@@ -44,6 +45,7 @@ class Workload:
     data_seed: int = 0
     rng_seed: int = 0              # Philox seed of the random eviction
     sm_scale: float = field(default=0.0)
+    protect: int = -1              # protected proxies; -1: all of them
 
     @property
     def scale(self):
@@ -59,7 +61,7 @@ class Workload:
 
     @property
     def n_protect(self):
-        return self.P
+        return self.P if self.protect < 0 else self.protect
 
     @property
     def Cp(self):
@@ -105,6 +107,11 @@ WORKLOADS = {
     "long_128k": Workload("long_128k", 1, 1, 32, 131072, 128, "bf16", 512,
                           Fraction(1, 5), PAPER_RANDOM_SHARE_20, True,
                           hh_frac=Fraction(1, 1000), data_seed=5),
+    # The H2O special case of the scoring rule (Section 5.1): every token a
+    # proxy, none protected, the budget filled by score alone.  A dense,
+    # MFMA-bound column sum over the whole causal attention matrix.
+    "h2o_4k": Workload("h2o_4k", 1, 4, 32, 4096, 128, "bf16", 4096,
+                       Fraction(1, 5), Fraction(0), True, data_seed=6, protect=0),
 }
 
 SWEEP_KEEP = (Fraction(1, 10), Fraction(1, 5), Fraction(1, 2))

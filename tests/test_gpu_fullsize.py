@@ -66,7 +66,8 @@ def _properties(w, F, keep):
 def _evict(w, layer):
     q, k, v = make_layer(w, layer, device="cuda")
     pos_dev = torch.tensor(w.proxy_pos, dtype=torch.int32, device="cuda")
-    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=w.scale, proxy_pos_dev=pos_dev)
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, n_protect=w.n_protect, sm_scale=w.scale,
+                                     proxy_pos_dev=pos_dev)
     ws = nacl.workspace(prob)
     F, keep, ko, vo = nacl.evict(prob, q, k, v, w.C, w.Cr, SAMPLE_SOFTMAX, w.rng_seed, layer, ws=ws)
     torch.cuda.synchronize()
@@ -129,6 +130,17 @@ def test_long_128k():
     _properties(w, F, keep)
     n = _check_heads(w, 0, q, k, v, F, keep, ko, vo, [(0, 0), (0, 29)], "128k")
     _say(f"  128k: {n} near-tie differences")
+
+
+def test_h2o_4k():
+    """The H2O case of the scoring rule: batch 4 x 32 heads x 4096 tokens, every token
+    a proxy (eight groups of 512 rows through the wide kernel, the API's proxy limit),
+    none protected, the budget filled by score alone."""
+    w = WORKLOADS["h2o_4k"]
+    q, k, v, F, keep, ko, vo = _evict(w, 0)
+    _properties(w, F, keep)
+    n = _check_heads(w, 0, q, k, v, F, keep, ko, vo, [(0, 0), (3, 17)], "h2o_4k")
+    _say(f"  h2o_4k: {n} near-tie differences")
 
 
 def test_size_limits():
