@@ -52,9 +52,10 @@ int q_group_of(const nacl_problem* p) { return p->q_group > 1 ? p->q_group : 1; 
 int rows_of(const nacl_problem* p) { return p->P * q_group_of(p); }
 
 struct Layout {
-  size_t cnt, pos, lse, part, keys, xhist, xcand, total;
+  size_t cnt, pos, lse, part, keys, colpart, xhist, xcand, total;
   int n_chunks;
   size_t sel_sync_word;   // first word of the selection's sync region inside the counter section
+  size_t chunk_cnt_word;  // first word of the proxy-split score's per-chunk arrival counters
   int n_counter_words;    // counter words cleared before the score kernel (all but the sticky word)
 };
 
@@ -67,9 +68,13 @@ Layout layout_of(const nacl_problem* p) {
   size_t off = 0;
   l.cnt = off;
   // header, the score's per-head counters, then the selection's ticket
-  // (padded to 64 words) and per-head round counters
+  // (padded to 64 words) and per-head round counters, then (long proxy
+  // lists) the score's per-chunk counters
+  const int psplit = nacl::score_psplit(p->dtype, p->D, rows_of(p));
+  const size_t split_chunks = (p->L + nacl::kSplitChunkKeys - 1) / nacl::kSplitChunkKeys;
   l.sel_sync_word = kCounterHeader + BH;
-  l.n_counter_words = (int)(kCounterHeader + BH + 64 + BH);
+  l.chunk_cnt_word = kCounterHeader + BH + 64 + BH;
+  l.n_counter_words = (int)(l.chunk_cnt_word + (psplit > 1 ? BH * split_chunks : 0));
   off += align_up((size_t)l.n_counter_words * sizeof(uint32_t));
   l.pos = off;
   off += align_up((size_t)p->P * sizeof(int32_t));
@@ -80,6 +85,8 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up(BH * l.n_chunks * rows * sizeof(float2));
   l.keys = off;
   off += align_up(BH * p->L * sizeof(uint32_t));
+  l.colpart = off;
+  if (psplit > 1) off += align_up(BH * split_chunks * psplit * nacl::kSplitChunkKeys * sizeof(float));
   // The sliced selection of long heads exchanges histograms and candidate
   // lists through these.
   const bool sliced = nacl::select_uses_slices(p->L);
@@ -256,12 +263,15 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   // The proxy-split kernel takes fixed items of kSplitChunkKeys keys.
   if (nacl::score_uses_split(p->dtype, p->D, rows_of(p))) sc.chunk_keys = nacl::kSplitChunkKeys;
   sc.n_chunks = (p->L + sc.chunk_keys - 1) / sc.chunk_keys;  // <= l.n_chunks
+  sc.n_psplit = nacl::score_psplit(p->dtype, p->D, rows_of(p));
+  sc.chunk_cnt = words + l.chunk_cnt_word;
+  sc.colpart = reinterpret_cast<float*>(ws + l.colpart);
   const int group_items = nacl::score_uses_split(p->dtype, p->D, rows_of(p)) ? NACL_SCORE_SPLIT_GROUP_ITEMS_PER_CU
                                                                        : NACL_SCORE_GROUP_ITEMS_PER_CU;
-  sc.heads_per_group = heads_per_group(BH, sc.n_chunks, group_items * cus);
+  sc.heads_per_group = heads_per_group(BH, sc.n_chunks * sc.n_psplit, group_items * cus);
   sc.n_groups = BH / sc.heads_per_group;
   sc.lag = std::min(NACL_SCORE_LAG, sc.n_groups);
-  sc.total_items = passes * BH * sc.n_chunks;
+  sc.total_items = passes * BH * sc.n_chunks * sc.n_psplit;
   sc.partials = reinterpret_cast<float2*>(ws + l.part);
   sc.lse2 = reinterpret_cast<float*>(ws + l.lse);
   sc.lse_in = lse;

@@ -47,6 +47,12 @@ constexpr int kScoreWaves = 4;  // waves per work-group, each owning a quarter o
 #endif
 constexpr int kSplitChunkKeys = NACL_SPLIT_CHUNK;
 inline bool score_uses_split(int dtype, int D, int P) { return NACL_SCORE_SPLIT && dtype == 1 && D == 128 && P >= 128; }
+// Proxy rows per group of the wide split kernel (from this many rows on it
+// is the one launched), and its items per chunk along the rows.
+constexpr int kSplitWideRows = 512;
+inline int score_psplit(int dtype, int D, int P) {
+  return score_uses_split(dtype, D, P) && P > kSplitWideRows ? (P + kSplitWideRows - 1) / kSplitWideRows : 1;
+}
 // The workspace is sized for the shortest item of either kernel.
 constexpr int kScoreMinChunkKeys = std::min(kScoreTpwMin * kScoreWaves * 16, kSplitChunkKeys);
 
@@ -68,6 +74,9 @@ struct ScoreSched {
   int n_groups;          // B*H / heads_per_group
   int lag;               // pass-2 items of group g follow pass-1 items of group g + lag
   int total_items;
+  int n_psplit;          // items per chunk along the proxy rows: 1, or one per group of
+                         // kSplitWideRows rows (long proxy lists; the column sums of a chunk
+                         // are then added in group order by the chunk's last item)
   int lse_given;         // 1: the caller supplied the log-sum-exp, only pass 2 runs
   uint32_t* queue;       // workspace counter words: queue, status, then per-head counters
   uint32_t* status;      // health words: [0] this call's, [1] sticky; bit 0 set if a pass-2
@@ -75,6 +84,8 @@ struct ScoreSched {
   uint32_t* head_cnt;    // [B*H]
   float2* partials;      // [B*H, n_chunks, P] base-2 (max, sum)
   float* lse2;           // [B*H, P] base-2 log-sum-exp
+  uint32_t* chunk_cnt;   // [B*H, n_chunks] arrivals of a chunk's items (n_psplit > 1)
+  float* colpart;        // [B*H, n_chunks, n_psplit, chunk_keys] per-group column sums (n_psplit > 1)
   const float* lse_in;   // caller's log-sum-exp when lse_given
   float lse_mul;         // log2(e) for a natural log-sum-exp
   float* scores;         // [B*H, L]

@@ -228,11 +228,13 @@ struct ItemRef {
   int kind;   // 1 = pass 1, 2 = pass 2
   int bh;
   int chunk;
+  int psl;    // group of proxy rows (0 unless the items are split along the rows)
 };
 
 // Item i of the queue order described at the top of the file.
 __device__ __forceinline__ ItemRef decode_item(const ScoreSched& s, int i) {
-  const int S = s.heads_per_group * s.n_chunks;  // items per group and pass
+  const int U = s.n_chunks * s.n_psplit;         // items per head and pass
+  const int S = s.heads_per_group * U;           // items per group and pass
   int kind, group, r;
   if (s.lse_given) {
     kind = 2;
@@ -262,7 +264,8 @@ __device__ __forceinline__ ItemRef decode_item(const ScoreSched& s, int i) {
       r = (i2 - mid) % S;
     }
   }
-  return ItemRef{kind, group * s.heads_per_group + r / s.n_chunks, r % s.n_chunks};
+  const int u = r % U;
+  return ItemRef{kind, group * s.heads_per_group + r / U, u / s.n_psplit, u % s.n_psplit};
 }
 
 // Proxy row r of a K/V head is proxy r / qg of query head r % qg of its
@@ -773,9 +776,7 @@ __global__ void score_init_kernel(uint32_t* words, int n) {
 #define NACL_SPLIT_OCC 4
 #endif
 // Proxy lists at least this long use groups of 512 (eight blocks per wave).
-#ifndef NACL_SPLIT_WIDE_P
-#define NACL_SPLIT_WIDE_P 512
-#endif
+constexpr int kSplitWideP = kSplitWideRows;
 constexpr int kSplitDepth = NACL_SPLIT_DEPTH;                // ring slots per block (at most 8)
 constexpr int kSplitTiles = kSplitChunkKeys / 16;            // tiles per item
 static_assert(kSplitTiles % kSplitDepth == 0 && kSplitDepth % 4 == 0, "tiles per item vs ring");
@@ -804,11 +805,12 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
   constexpr int kSplitGroup = 16 * WB * kScoreWaves;  // proxies per group
   constexpr int kNB = WB < 4 ? WB : 4;                // proxy blocks per MFMA batch
   static_assert(KS::kInstr == kScoreWaves, "one DMA instruction per wave and tile");
+  static_assert(WB != 8 || kSplitGroup == kSplitWideRows, "row groups of split items are the wide kernel's groups");
   __shared__ int item_s, last_s;
   __shared__ int pos_g[kSplitGroup];
   __shared__ int64_t qrow_g[kSplitGroup];  // element offset of each row's query from qb
   __shared__ float2 mrg[kScoreThreads];
-  __shared__ float col_lds[kSplitChunkKeys];
+  __shared__ __attribute__((aligned(16))) float col_lds[kSplitChunkKeys];
   __shared__ float stage[kScoreWaves][64];
   __shared__ __attribute__((aligned(16))) float lse_g[kSplitGroup];
 #define NACL_SSLOT(i) __shared__ __attribute__((aligned(16))) unsigned char sslot##i[KS::kTileBytes];
@@ -917,13 +919,16 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
       }
     };
 
+    // The item's proxy rows [gb, ge): every row, or one group of them.
+    const int gb = s.n_psplit > 1 ? it.psl * kSplitGroup : 0;
+    const int ge = s.n_psplit > 1 ? min(a.P, gb + kSplitGroup) : a.P;
     if (it.kind == 1) {
       // ---------------- pass 1: per-chunk (reference, sum) of every proxy row
       float2* part = s.partials + ((int64_t)bh * s.n_chunks + it.chunk) * a.P;
       if (beyond)
-        for (int i = threadIdx.x; i < a.P; i += kScoreThreads)
+        for (int i = gb + threadIdx.x; i < ge; i += kScoreThreads)
           store_coherent(part + i, make_float2(-INFINITY, 0.f));
-      for (int g0 = 0; g0 < (beyond ? 0 : a.P); g0 += kSplitGroup) {
+      for (int g0 = gb; g0 < (beyond ? gb : ge); g0 += kSplitGroup) {
         const int gn = min(kSplitGroup, a.P - g0);
         load_group(g0, gn);
         if (pos_g[gn - 1] < chunk_key0) {
@@ -1047,7 +1052,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
       // Publish the partials; the last chunk of the head merges them.
       wait_stores();
       __syncthreads();
-      if (threadIdx.x == 0) last_s = atomicAdd(&s.head_cnt[bh], 1u) == (unsigned)(s.n_chunks - 1);
+      if (threadIdx.x == 0) last_s = atomicAdd(&s.head_cnt[bh], 1u) == (unsigned)(s.n_chunks * s.n_psplit - 1);
       __syncthreads();
       if (last_s) {
         const float2* hp = s.partials + (int64_t)bh * s.n_chunks * a.P;
@@ -1085,16 +1090,18 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
         if (threadIdx.x == 0) atomicAdd(&s.head_cnt[bh], 1u);
       }
     } else if (beyond) {
-      float* F = s.scores + (int64_t)bh * a.L;
-      const int end = min(chunk_key0 + kSplitChunkKeys, a.L);
-      for (int j = chunk_key0 + threadIdx.x; j < end; j += kScoreThreads) F[j] = 0.f;
-      if (s.gkeys) chunk_gumbel_keys([](int) { return 0.f; });
+      if (it.psl == 0) {
+        float* F = s.scores + (int64_t)bh * a.L;
+        const int end = min(chunk_key0 + kSplitChunkKeys, a.L);
+        for (int j = chunk_key0 + threadIdx.x; j < end; j += kScoreThreads) F[j] = 0.f;
+        if (s.gkeys) chunk_gumbel_keys([](int) { return 0.f; });
+      }
     } else {
       // ---------------- pass 2: column sums of exp2(logit - LSE) ----------
       if (!s.lse_given) {
         if (threadIdx.x == 0) {
           uint32_t spins = 0;
-          while (load_coherent(&s.head_cnt[bh]) < (unsigned)(s.n_chunks + 1)) {
+          while (load_coherent(&s.head_cnt[bh]) < (unsigned)(s.n_chunks * s.n_psplit + 1)) {
             __builtin_amdgcn_s_sleep(2);
             if (++spins > kSpinLimit) {
               atomicOr(s.status, 1u);
@@ -1108,7 +1115,7 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
       const float* lse = s.lse_given ? s.lse_in : s.lse2;
       const float lse_mul = s.lse_given ? s.lse_mul : 1.0f;
       bool fresh = true;  // the item's columns are not yet written
-      for (int g0 = 0; g0 < a.P; g0 += kSplitGroup) {
+      for (int g0 = gb; g0 < ge; g0 += kSplitGroup) {
         const int gn = min(kSplitGroup, a.P - g0);
         load_group(g0, gn);
         if (pos_g[gn - 1] < chunk_key0) continue;  // no row of the group sees this chunk
@@ -1193,13 +1200,44 @@ __device__ __forceinline__ void score_split_body(const __bf16* __restrict__ q, c
         fresh = false;
       }
       __syncthreads();
-      float* F = s.scores + (int64_t)bh * a.L;
-      auto col_of = [&](int idx) -> float { return col_lds[idx]; };
-      for (int idx = threadIdx.x; idx < kSplitChunkKeys; idx += kScoreThreads) {
-        const int key = chunk_key0 + idx;
-        if (key < a.L) F[key] = col_of(idx);
+      bool write = true;
+      if (s.n_psplit > 1) {
+        // Publish this group's column sums (none if no row of it sees the
+        // chunk); the chunk's last item adds the groups' sums in group order,
+        // as one item over every group would, and writes the scores.
+        const int64_t cidx = (int64_t)bh * s.n_chunks + it.chunk;
+        float* cp = s.colpart + cidx * s.n_psplit * kSplitChunkKeys;
+        if (!fresh)
+          for (int q4 = 4 * (int)threadIdx.x; q4 < kSplitChunkKeys; q4 += 4 * kScoreThreads)
+            store_coherent16(cp + it.psl * kSplitChunkKeys + q4,
+                             __builtin_bit_cast(u32x4, *reinterpret_cast<const f32x4*>(col_lds + q4)));
+        wait_stores();
+        __syncthreads();
+        if (threadIdx.x == 0) last_s = atomicAdd(&s.chunk_cnt[cidx], 1u) == (unsigned)(s.n_psplit - 1);
+        __syncthreads();
+        write = last_s != 0;
+        if (write) {
+          for (int idx = threadIdx.x; idx < kSplitChunkKeys; idx += kScoreThreads) {
+            float acc = 0.f;
+            for (int pg = 0; pg < s.n_psplit; ++pg) {
+              int64_t unused;
+              const int lr = min(a.P, (pg + 1) * kSplitGroup) - 1;  // the group's last row
+              if (row_position(a, lr, unused) >= chunk_key0) acc += load_coherent(cp + pg * kSplitChunkKeys + idx);
+            }
+            col_lds[idx] = acc;
+          }
+          __syncthreads();
+        }
       }
-      if (s.gkeys) chunk_gumbel_keys(col_of);
+      if (write) {
+        float* F = s.scores + (int64_t)bh * a.L;
+        auto col_of = [&](int idx) -> float { return col_lds[idx]; };
+        for (int idx = threadIdx.x; idx < kSplitChunkKeys; idx += kScoreThreads) {
+          const int key = chunk_key0 + idx;
+          if (key < a.L) F[key] = col_of(idx);
+        }
+        if (s.gkeys) chunk_gumbel_keys(col_of);
+      }
     }
   }
 }
@@ -1270,15 +1308,17 @@ hipError_t launch_score_split_t(K kern, const ScoreLaunch& L, hipStream_t stream
 }
 
 hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
-  if (L.args.P >= NACL_SPLIT_WIDE_P) return launch_score_split_t(score_split_wide_kernel, L, stream);
+  if (L.args.P >= kSplitWideP) return launch_score_split_t(score_split_wide_kernel, L, stream);
   return launch_score_split_t(score_split_kernel, L, stream);
 }
 
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream) {
   if (score_uses_split(L.dtype, L.D, L.args.P)) {
     if (L.sched.chunk_keys != kSplitChunkKeys) return hipErrorInvalidValue;
+    if (L.sched.n_psplit != score_psplit(L.dtype, L.D, L.args.P)) return hipErrorInvalidValue;
     return launch_score_split(L, stream);
   }
+  if (L.sched.n_psplit != 1) return hipErrorInvalidValue;
   const int pb = proxy_blocks(L.dtype, L.D, L.args.P);
   if (L.dtype == 1) {
     if (L.D == 128) {

@@ -655,12 +655,6 @@ struct SliceLds {
   uint32_t list[kSelSlice];       // this slice's kept indices, in order
 };
 
-// store_coherent's 16-byte form: a vector store at the device coherence
-// point (sc1), made complete by wait_stores() like the others.
-__device__ __forceinline__ void store_coherent16(uint32_t* p, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
-}
-
 // Sum over the wave.
 __device__ __forceinline__ uint32_t wave_sum(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_readlane((int)wave_inclusive_scan(x), kWave - 1);
