@@ -51,8 +51,10 @@ int elt_bytes(int dtype) { return dtype == NACL_F32 ? 4 : 2; }
 int q_group_of(const nacl_problem* p) { return p->q_group > 1 ? p->q_group : 1; }
 int rows_of(const nacl_problem* p) { return p->P * q_group_of(p); }
 
+int logits_stride(const nacl_problem* p) { return (p->L + 3) / 4 * 4; }
+
 struct Layout {
-  size_t cnt, pos, lse, part, keys, colpart, xhist, xcand, total;
+  size_t cnt, pos, lse, part, keys, colpart, logits, xhist, xcand, total;
   int n_chunks;
   size_t sel_sync_word;   // first word of the selection's sync region inside the counter section
   size_t chunk_cnt_word;  // first word of the proxy-split score's per-chunk arrival counters
@@ -64,7 +66,8 @@ constexpr int kCounterHeader = 64;  // queue + status words, padded to 256 bytes
 Layout layout_of(const nacl_problem* p) {
   Layout l;
   const size_t BH = (size_t)p->B * p->H;
-  l.n_chunks = (p->L + nacl::kScoreMinChunkKeys - 1) / nacl::kScoreMinChunkKeys;  // most chunks any call uses
+  const int min_chunk = nacl::score_uses_rows(p->dtype, p->D, rows_of(p)) ? nacl::kRowsChunkMin : nacl::kScoreMinChunkKeys;
+  l.n_chunks = (p->L + min_chunk - 1) / min_chunk;  // most chunks any call uses
   size_t off = 0;
   l.cnt = off;
   // header, the score's per-head counters, then the selection's ticket
@@ -87,6 +90,10 @@ Layout layout_of(const nacl_problem* p) {
   off += align_up(BH * p->L * sizeof(uint32_t));
   l.colpart = off;
   if (psplit > 1) off += align_up(BH * split_chunks * psplit * nacl::kSplitChunkKeys * sizeof(float));
+  // Few proxy rows: every key's logits, rows padded to a multiple of 4 keys.
+  l.logits = off;
+  if (nacl::score_uses_rows(p->dtype, p->D, (int)rows))
+    off += align_up(BH * rows * (size_t)logits_stride(p) * sizeof(float));
   // The sliced selection of long heads exchanges histograms and candidate
   // lists through these.
   const bool sliced = nacl::select_uses_slices(p->L);
@@ -276,6 +283,14 @@ int run_score(const nacl_problem* p, const void* q, const void* k, const float* 
   sc.lse2 = reinterpret_cast<float*>(ws + l.lse);
   sc.lse_in = lse;
   sc.lse_mul = 1.4426950408889634f;
+  if (!sc.lse_given && nacl::score_uses_rows(p->dtype, p->D, rows_of(p))) {
+    // Few proxy rows: K is read once and the logits are kept (see score.hip).
+    sc.logits = reinterpret_cast<float*>(ws + l.logits);
+    sc.logits_stride = logits_stride(p);
+    sc.chunk_keys = nacl::score_rows_chunk(p->dtype, p->D, p->L, BH, cus);
+    sc.n_chunks = (p->L + sc.chunk_keys - 1) / sc.chunk_keys;  // <= l.n_chunks
+    for (int r = 0; r < rows_of(p); ++r) sc.row_pos[r] = p->proxy_pos[r / q_group_of(p)];
+  }
   hipError_t e = nacl::launch_score(s, stream);
   if (e != hipSuccess) return hip_fail(e, "score kernel");
   return NACL_OK;

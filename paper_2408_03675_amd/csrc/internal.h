@@ -53,7 +53,21 @@ constexpr int kSplitWideRows = 512;
 inline int score_psplit(int dtype, int D, int P) {
   return score_uses_split(dtype, D, P) && P > kSplitWideRows ? (P + kSplitWideRows - 1) / kSplitWideRows : 1;
 }
-// The workspace is sized for the shortest item of either kernel.
+// Few proxy rows (one query row per head in generation-phase eviction, the
+// single-token proxy set): the logits of every key are kept in the workspace
+// (4 bytes per row and key) instead of reading K again, as long as that is
+// cheaper than the second read of a K row.  A work-group of the logit kernel
+// takes a chunk of 64 * t keys (t tiles of 16 keys per wave), at most
+// kRowsChunkMax, and at least kRowsChunkMin unless the head is shorter.
+constexpr int kRowsChunkMax = 1024;
+constexpr int kRowsChunkMin = 256;
+inline int score_rows_max(int dtype, int D) { return D * (dtype == 0 ? 4 : 2) >= 256 ? 16 : 8; }
+inline bool score_uses_rows(int dtype, int D, int P) { return P <= score_rows_max(dtype, D); }
+// Chunk length of the logit kernel for B*H heads of L keys: the fewest
+// rounds of resident work-groups, the chunks sized to fill them.
+int score_rows_chunk(int dtype, int D, int L, int BH, int cus);
+// The workspace is sized for the shortest item of either queue kernel (and
+// for kRowsChunkMin-key chunks on the few-row path).
 constexpr int kScoreMinChunkKeys = std::min(kScoreTpwMin * kScoreWaves * 16, kSplitChunkKeys);
 
 struct ScoreArgs {
@@ -86,6 +100,9 @@ struct ScoreSched {
   float* lse2;           // [B*H, P] base-2 log-sum-exp
   uint32_t* chunk_cnt;   // [B*H, n_chunks] arrivals of a chunk's items (n_psplit > 1)
   float* colpart;        // [B*H, n_chunks, n_psplit, chunk_keys] per-group column sums (n_psplit > 1)
+  float* logits;         // few-row path (nullptr otherwise): [B*H, P, logits_stride] raw logits
+  int logits_stride;     // L rounded up to a multiple of 4
+  int row_pos[16];       // few-row path: position of row r (proxy r / qg), from the host
   const float* lse_in;   // caller's log-sum-exp when lse_given
   float lse_mul;         // log2(e) for a natural log-sum-exp
   float* scores;         // [B*H, L]

@@ -444,9 +444,11 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
         static_for<kUnroll>([&](auto u_c) {
           constexpr int u = decltype(u_c)::value;
           const int tt = t + u;
-          // The slot of tile tt - 1 was read (and its reads retired) in the
-          // previous step: refill it before waiting, so kDepth - 1 tiles stay
-          // in flight across the wait.
+          // The slot of tile tt - 1 was read in the previous step: refill it
+          // before waiting, so kDepth - 1 tiles stay in flight across the
+          // wait.  The LDS wait first makes those reads complete (the
+          // compiler may otherwise issue the refill while some are queued).
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
           KS::issue(rsrc, vo, tile_byte(tt + kDepth - 1), slot(std::integral_constant<int, u + kDepth - 1>{}));
           asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KS::kInstr * (kDepth - 1)) : "memory");
           frag_t kf[kS];
@@ -755,6 +757,227 @@ __attribute__((amdgpu_waves_per_eu(kScoreWavesPerSimd, kScoreWavesPerSimd))) voi
 __global__ void score_init_kernel(uint32_t* words, int n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
     if (i != 2) words[i] = 0u;
+}
+
+// ---------------------------------------------------------------------------
+// Few proxy rows (at most score_rows_max rows per K/V head, log-sum-exp
+// computed here).  With one to sixteen rows a key's logits take 4 to 64
+// bytes, less than its K row, so they are stored instead of reading K again:
+//   score_rows_logits_kernel  one work-group per chunk of a head (64 to
+//     kRowsChunkMax keys, sized so that the work-groups fill whole rounds of
+//     the resident ones); each wave streams a quarter of it through its own LDS
+//     ring (buffer loads that write LDS, as in the kernels above), computes
+//     their logits (16 keys per MFMA tile, rows = keys, columns = the proxy
+//     rows) and keeps them in registers; then it stores them and the
+//     chunk's base-2 (maximum, sum) per row, taken against the chunk's exact
+//     maximum, so no term exceeds 1;
+//   score_rows_column_kernel  merges a head's partials into its log-sum-exp
+//     (each work-group of the head for itself), then F[j] = sum over the
+//     rows that see key j of exp2(logit * c2 - LSE) from the stored logits
+//     (rows in order), and inside a whole eviction the Gumbel keys of the
+//     four keys a thread owns.
+// No work-group waits for another: no queue, no counter, no spin.
+
+template <typename T, int D>
+__global__ __launch_bounds__(kScoreThreads) void score_rows_logits_kernel(const T* __restrict__ q,
+                                                                         const T* __restrict__ k, ScoreArgs a,
+                                                                         ScoreSched s) {
+  using M = Mma<T, D>;
+  using frag_t = typename M::frag_t;
+  using KS = KStage<T, D>;
+  constexpr int kS = M::kSteps;
+  constexpr int kTiles = kRowsChunkMax / 16 / kScoreWaves;  // most tiles of 16 keys per wave
+  // Ring slots per wave: 12 KB of tiles (at least two), so that three
+  // work-groups share a CU's LDS.
+  constexpr int kDepth = 12288 / KS::kTileBytes < 2 ? 2 : (12288 / KS::kTileBytes > 8 ? 8 : 12288 / KS::kTileBytes);
+  __shared__ float red[kScoreWaves][16];
+  // One array per ring slot, so that the compiler sees a DMA into one slot
+  // does not alias reads of another.
+#define NACL_RSLOT(i) \
+  __shared__ __attribute__((aligned(16))) unsigned char rslot##i[kScoreWaves][kDepth > i ? KS::kTileBytes : 16];
+  NACL_RSLOT(0) NACL_RSLOT(1) NACL_RSLOT(2) NACL_RSLOT(3) NACL_RSLOT(4) NACL_RSLOT(5) NACL_RSLOT(6) NACL_RSLOT(7)
+#undef NACL_RSLOT
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int chunk = blockIdx.x, bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  const int tpw = s.chunk_keys / (16 * kScoreWaves);  // this launch's tiles per wave, 1 .. kTiles
+  const int key_c0 = chunk * s.chunk_keys;
+  float2* part = s.partials + ((int64_t)bh * s.n_chunks + chunk) * a.P;
+  const float c2 = a.c2;
+  if (key_c0 > a.p_last) {
+    // No row sees these keys: an empty partial, no logits.
+    for (int i = threadIdx.x; i < a.P; i += kScoreThreads) part[i] = make_float2(-INFINITY, 0.f);
+  } else {
+    // This lane's proxy row r16 (none past the last row: position -1, so no
+    // key is visible to it; positions come with the launch) and its query
+    // fragments, loaded before the K stream (vector memory loads complete in
+    // order, so the stream's waits cover them).
+    const bool row_ok = r16 < a.P;
+    const int pr = row_ok ? s.row_pos[r16] : -1;
+    frag_t qf[kS];
+    const T* qb = q + b * a.qs[0] + (int64_t)h * a.qg * a.qs[1];
+    if (row_ok) M::load(qb + (int64_t)(r16 % a.qg) * a.qs[1] + (int64_t)pr * a.qs[2], g, qf);
+    else M::zero(qf);
+    const T* kb = k + b * a.ks[0] + h * a.ks[1];
+    const uint32_t row_bytes = (uint32_t)(a.ks[2] * (int64_t)sizeof(T));
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(kb), (short)0, (int)((uint32_t)(a.L - 1) * row_bytes + (uint32_t)(D * sizeof(T))),
+        kBufferRsrcWord3);
+    uint32_t vo[KS::kInstr];
+    KS::offsets(row_bytes, lane, vo);
+    const int key_w0 = key_c0 + wave * tpw * 16;  // the wave's tpw * 16 consecutive keys
+    // Tiles past the wave's range or past L get an offset beyond the
+    // descriptor: the DMA reads zeros without touching memory, so every
+    // wait count below is static.
+    auto tile_byte = [&](int t) -> uint32_t {
+      const int key0 = key_w0 + 16 * t;
+      return t < tpw && key0 < a.L ? (uint32_t)key0 * row_bytes : kOutOfRange;
+    };
+    auto slot = [&](auto u_c) -> unsigned char* {
+      constexpr int u = decltype(u_c)::value % kDepth;
+      if constexpr (u == 0) return rslot0[wave];
+      else if constexpr (u == 1) return rslot1[wave];
+      else if constexpr (u == 2) return rslot2[wave];
+      else if constexpr (u == 3) return rslot3[wave];
+      else if constexpr (u == 4) return rslot4[wave];
+      else if constexpr (u == 5) return rslot5[wave];
+      else if constexpr (u == 6) return rslot6[wave];
+      else return rslot7[wave];
+    };
+    // The wave's logits stay in registers (lg[t][e]: key key_w0 + 16 t +
+    // 4 g + e, row r16) until the stream ends; the stream issues no other
+    // vector memory operation, so its wait counts are exact.
+    f32x4 lg[kTiles];
+    static_for<kDepth - 1>([&](auto u_c) { KS::issue(rsrc, vo, tile_byte(decltype(u_c)::value), slot(u_c)); });
+    static_for<kTiles>([&](auto t_c) {
+      constexpr int t = decltype(t_c)::value;
+      // The slot of tile t - 1 was read in the previous step: refill it
+      // before waiting, so kDepth - 1 tiles stay in flight.  The LDS wait
+      // first makes those reads complete (the compiler may otherwise issue
+      // the refill while the last of them are still queued).
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      KS::issue(rsrc, vo, tile_byte(t + kDepth - 1), slot(std::integral_constant<int, t + kDepth - 1>{}));
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(KS::kInstr * (kDepth - 1)) : "memory");
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if (t < tpw) {
+        frag_t kf[kS];
+        KS::template frag<M>(slot(t_c), r16, g, kf);
+#pragma unroll
+        for (int ks = 0; ks < kS; ++ks) acc = M::mma(kf[ks], qf[ks], acc);
+      }
+      lg[t] = acc;
+    });
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // Store the logits (the row stride is a multiple of 4, so a group of four
+    // keys reaching past L stays in the row's padding).
+    if (row_ok) {
+      float* lrow = s.logits + ((int64_t)bh * a.P + r16) * s.logits_stride;
+#pragma unroll
+      for (int t = 0; t < kTiles; ++t) {
+        const int key = key_w0 + 16 * t + 4 * g;
+        if (t < tpw && key < a.L) *reinterpret_cast<f32x4*>(lrow + key) = lg[t];
+      }
+    }
+    // The chunk's maximum per row over the keys the row sees (a prefix of
+    // the keys), then the sum of exp2(logit * c2 - maximum * c2).
+    // Keys of tiles past tpw belong to the next wave: none counts here.
+    const int pw = min(pr, key_w0 + 16 * tpw - 1);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mx = key_w0 + 16 * t + 4 * g + e <= pw ? fmaxf(mx, lg[t][e]) : mx;
+    mx = max_over_groups(mx);
+    if (g == 0) red[wave][r16] = mx;
+    __syncthreads();
+    float bm = red[0][r16];
+#pragma unroll
+    for (int w = 1; w < kScoreWaves; ++w) bm = fmaxf(bm, red[w][r16]);
+    const float ref = bm != -INFINITY ? bm * c2 : 0.f;
+    float sm = 0.f;
+#pragma unroll
+    for (int t = 0; t < kTiles; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        sm += key_w0 + 16 * t + 4 * g + e <= pw ? fast_exp2(fmaf(lg[t][e], c2, -ref)) : 0.f;
+    sm = sum_over_groups(sm);
+    __syncthreads();  // every wave has read red
+    if (g == 0) red[wave][r16] = sm;
+    __syncthreads();
+    // Thread r < P (lane r of wave 0) holds row r's reference.
+    if (threadIdx.x < a.P) {
+      const int r = threadIdx.x;
+      const float tot = ((red[0][r] + red[1][r]) + red[2][r]) + red[3][r];
+      part[r] = tot > 0.f ? make_float2(ref, tot) : make_float2(-INFINITY, 0.f);
+    }
+  }
+}
+
+__global__ __launch_bounds__(kScoreThreads) void score_rows_column_kernel(ScoreArgs a, ScoreSched s) {
+  __shared__ float lse_s[16];
+  __shared__ int pos_s[16];
+  __shared__ float2 mrg[kScoreThreads];
+  const int bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  {
+    // The head's log-sum-exp per row from the chunks' partials (every
+    // work-group of the head merges them itself): `split` threads share a
+    // row, each taking every split-th chunk with kMB loads in flight, and
+    // they combine through LDS in thread order.
+    const float2* hp = s.partials + (int64_t)bh * s.n_chunks * a.P;
+    constexpr int kMB = 8;
+    // Enough threads per row for one batch of kMB loads each, at most
+    // kScoreThreads / P (the combine below is serial in split).
+    const int split = min(kScoreThreads / a.P, (s.n_chunks + kMB - 1) / kMB);
+    const int i = (int)threadIdx.x % a.P, pi = (int)threadIdx.x / a.P;
+    float mm = -INFINITY, ss = 0.f;
+    if (pi < split) {
+      for (int c0 = pi; c0 < s.n_chunks; c0 += kMB * split) {
+        float2 v[kMB];
+#pragma unroll
+        for (int u = 0; u < kMB; ++u) {
+          const int c = c0 + u * split;
+          v[u] = c < s.n_chunks ? hp[(int64_t)c * a.P + i] : make_float2(-INFINITY, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < kMB; ++u) lse_merge(mm, ss, v[u].x, v[u].y);
+      }
+    }
+    mrg[threadIdx.x] = make_float2(mm, ss);
+    __syncthreads();
+    if (threadIdx.x < a.P) {
+      for (int pp = 1; pp < split; ++pp) {
+        const float2 r = mrg[threadIdx.x + pp * a.P];
+        lse_merge(mm, ss, r.x, r.y);
+      }
+      const float l2 = mm + __log2f(ss);
+      lse_s[threadIdx.x] = l2;
+      pos_s[threadIdx.x] = s.row_pos[threadIdx.x];
+      if (blockIdx.x == 0) s.lse2[(int64_t)bh * a.P + threadIdx.x] = l2;
+    }
+    __syncthreads();
+  }
+  const int j0 = 4 * (blockIdx.x * kScoreThreads + (int)threadIdx.x);
+  if (j0 >= a.L) return;
+  const int n = min(4, a.L - j0);
+  float fv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j0 <= a.p_last) {
+    for (int r = 0; r < a.P; ++r) {
+      const int pr = pos_s[r];
+      if (j0 > pr) continue;  // the row sees none of the four keys
+      const f32x4 x = *reinterpret_cast<const f32x4*>(s.logits + ((int64_t)bh * a.P + r) * s.logits_stride + j0);
+      const float l2 = lse_s[r];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) fv[e] += j0 + e <= pr ? fast_exp2(fmaf(x[e], a.c2, -l2)) : 0.f;
+    }
+  }
+  float* F = s.scores + (int64_t)bh * a.L + j0;
+  for (int e = 0; e < n; ++e) F[e] = fv[e];
+  if (s.gkeys) {
+    uint32_t kv[4];
+    gumbel_block_keys(s.g_mode, j0, n, b, h, s.g_layer, s.g_k0, s.g_k1, fv, kv);
+    uint32_t* gk = s.gkeys + (int64_t)bh * a.L + j0;
+    for (int e = 0; e < n; ++e) gk[e] = kv[e];
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1312,7 +1535,55 @@ hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
   return launch_score_split_t(score_split_kernel, L, stream);
 }
 
+template <typename T, int D>
+hipError_t launch_score_rows_t(const ScoreLaunch& L, hipStream_t stream) {
+  const ScoreSched& s = L.sched;
+  const int BH = L.args.B * L.args.H;
+  const int init_blocks = std::max(1, std::min(64, (L.n_counter_words + 255) / 256));
+  hipLaunchKernelGGL(score_init_kernel, dim3(init_blocks), dim3(256), 0, stream, s.queue, L.n_counter_words);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((score_rows_logits_kernel<T, D>), dim3(s.n_chunks, BH), dim3(kScoreThreads), 0, stream,
+                     static_cast<const T*>(L.q), static_cast<const T*>(L.k), L.args, s);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int col_blocks = (L.args.L + 4 * kScoreThreads - 1) / (4 * kScoreThreads);
+  hipLaunchKernelGGL(score_rows_column_kernel, dim3(col_blocks, BH), dim3(kScoreThreads), 0, stream, L.args, s);
+  return hipGetLastError();
+}
+
+int score_rows_chunk(int dtype, int D, int L, int BH, int cus) {
+  int per_cu = 0;
+  hipError_t e;
+  if (dtype == 1)
+    e = D == 128 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_rows_logits_kernel<__bf16, 128>, kScoreThreads, 0)
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_rows_logits_kernel<__bf16, 64>, kScoreThreads, 0);
+  else
+    e = D == 128 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_rows_logits_kernel<float, 128>, kScoreThreads, 0)
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_rows_logits_kernel<float, 64>, kScoreThreads, 0);
+  if (e != hipSuccess || per_cu < 1) per_cu = 1;
+  const int64_t slots = (int64_t)per_cu * std::max(1, cus);
+  // Fewest chunks per head (longest chunks), the rounds of resident
+  // work-groups they take, then as many chunks as fill those rounds.
+  const int64_t n_min = (L + kRowsChunkMax - 1) / kRowsChunkMax;
+  const int64_t rounds = (BH * n_min + slots - 1) / slots;
+  const int64_t n_fill = std::max(n_min, rounds * slots / BH);
+  int ck = (int)(((L + n_fill - 1) / n_fill + 63) / 64 * 64);
+  ck = std::max(ck, std::min(kRowsChunkMin, (L + 63) / 64 * 64));
+  return std::min(ck, kRowsChunkMax);
+}
+
 hipError_t launch_score(const ScoreLaunch& L, hipStream_t stream) {
+  if (L.sched.logits) {
+    // The few-row path: every row in one 16-column MFMA tile, one partial
+    // per chunk, no caller log-sum-exp.
+    const int ck = L.sched.chunk_keys;
+    if (!score_uses_rows(L.dtype, L.D, L.args.P) || L.args.P > 16 || L.sched.lse_given || ck < 64 ||
+        ck > kRowsChunkMax || ck % 64 != 0 || L.sched.n_chunks != (L.args.L + ck - 1) / ck ||
+        L.sched.logits_stride < L.args.L || L.sched.logits_stride % 4 != 0)
+      return hipErrorInvalidValue;
+    if (L.dtype == 1) return L.D == 128 ? launch_score_rows_t<__bf16, 128>(L, stream) : launch_score_rows_t<__bf16, 64>(L, stream);
+    return L.D == 128 ? launch_score_rows_t<float, 128>(L, stream) : launch_score_rows_t<float, 64>(L, stream);
+  }
   if (score_uses_split(L.dtype, L.D, L.args.P)) {
     if (L.sched.chunk_keys != kSplitChunkKeys) return hipErrorInvalidValue;
     if (L.sched.n_psplit != score_psplit(L.dtype, L.D, L.args.P)) return hipErrorInvalidValue;

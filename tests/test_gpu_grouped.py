@@ -38,6 +38,11 @@ CASES = [
     ("wide_rows640", 1, 2, 8, 2500, 128, "bf16", 80),
     ("kv8_q32_4k", 1, 8, 4, 4096, 128, "bf16", 64),
     ("tile_d64_bf16", 2, 3, 3, 1037, 64, "bf16", 30),
+    # few rows (K read once, logits kept): the decode case (one proxy, the group's
+    # query heads as rows), sixteen rows, fp32 with nine rows
+    ("rows_decode_g4", 2, 4, 4, 3001, 128, "bf16", 1),
+    ("rows16_g8", 1, 2, 8, 2000, 128, "bf16", 2),
+    ("rows9_f32_d64_g3", 1, 3, 3, 1500, 64, "f32", 3),
 ]
 
 

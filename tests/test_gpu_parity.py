@@ -73,6 +73,15 @@ SCORE_CASES = [
     ("bf16_wide_three_groups", 1, 1, 2300, 128, "bf16", list(range(1200, 2300))),
     ("f32_many_proxies", 1, 2, 1500, 64, "f32", list(range(800, 1500))),
     ("bf16_d64_three_groups", 1, 2, 1200, 64, "bf16", list(range(900, 1200))),
+    # few proxy rows (K read once, logits kept): one row at the last token over several
+    # 512-key chunks with a ragged tail, the most rows each element size takes, rows whose
+    # positions leave whole chunks unseen, and a head shorter than one tile
+    ("bf16_rows_last_token", 2, 3, 6617, 128, "bf16", [6616]),
+    ("bf16_rows16_spread", 1, 2, 5001, 128, "bf16", [40 + 311 * i for i in range(16)]),
+    ("bf16_d64_rows8", 2, 2, 1500, 64, "bf16", [3, 100, 511, 512, 513, 900, 1400, 1499]),
+    ("f32_d64_rows16", 1, 2, 2049, 64, "f32", list(range(700, 716))),
+    ("f32_d128_rows_early", 2, 1, 3000, 128, "f32", [10, 20, 600]),
+    ("bf16_rows_short", 1, 2, 13, 128, "bf16", [2, 12]),
 ]
 
 
@@ -348,7 +357,7 @@ def test_evict_is_deterministic():
 
 @pytest.mark.parametrize("mode", [SAMPLE_SOFTMAX, SAMPLE_PROPORTIONAL, SAMPLE_UNIFORM])
 @pytest.mark.parametrize("where", ["end", "early"])
-@pytest.mark.parametrize("P", [40, 128, 160])
+@pytest.mark.parametrize("P", [1, 6, 40, 128, 160])
 def test_evict_draws_the_same_keys_as_select(mode, where, P):
     """nacl_evict draws the Gumbel keys inside the column reduction (skipping
     the selection's key kernel); its keep set must equal that of nacl_select
@@ -357,7 +366,8 @@ def test_evict_draws_the_same_keys_as_select(mode, where, P):
     0, keys drawn on the zero path); L not a multiple of 4; every non-protected
     slot random, so every key's value matters.  P = 160 runs the proxy-split
     score kernel on one proxy group (P = 128) and on a full and a partial group
-    (P = 160), P = 40 the per-wave-tile one."""
+    (P = 160), P = 40 the per-wave-tile one, P = 1 and 6 the few-row path
+    (keys drawn by its column kernel)."""
     B, H, L, D = 2, 3, 9001, 128
     pos = list(range(L - P, L)) if where == "end" else list(range(300, 300 + P))
     _say("evict keys", mode, where, P)
