@@ -257,7 +257,8 @@ def run_generation(name, m_steps=(16, 64, 256)):
     """Generation-phase eviction (Section 3; Algorithm 1, Generation) at decode
     shapes: the cache of one layer holds C kept entries per head plus m decoding
     steps; a round appends the m new K/V rows (nacl_append) and evicts the
-    C + m cache back to C in place with the current token as the only proxy.
+    C + m cache back to C in place with the current token as the only proxy,
+    in token order (nacl_evict) and in the slot form (nacl_evict_slots).
     Events around ten back-to-back rounds, median of three such runs; one JSON
     line per m."""
     import statistics
@@ -294,6 +295,19 @@ def run_generation(name, m_steps=(16, 64, 256)):
             nacl.evict(prob, q_cur, kc, vc, w.C, Cr, nacl.SAMPLE_SOFTMAX, seed, 0, ws=ws, scores=F,
                        keep_idx=keep, in_place=True)
 
+        # The slot form: kept rows stay in their slots, only the kept rows
+        # among the m new ones move (nacl_evict_slots).
+        slots = torch.empty((w.B, w.H, w.C), dtype=torch.int32, device=dev)
+
+        def rnd_slots(seed):
+            nacl.append(prob, kc, vc, w.C, k_new, v_new)
+            nacl.evict_slots(prob, q_cur, kc, vc, w.C, Cr, nacl.SAMPLE_SOFTMAX, seed, 0, ws=ws, scores=F,
+                             keep_idx=keep, slot_idx=slots)
+
+        def evict_slots_only(seed):
+            nacl.evict_slots(prob, q_cur, kc, vc, w.C, Cr, nacl.SAMPLE_SOFTMAX, seed, 0, ws=ws, scores=F,
+                             keep_idx=keep, slot_idx=slots)
+
         def med(fn, reps=10, rounds=3):
             for i in range(3):
                 fn(i)
@@ -310,14 +324,18 @@ def run_generation(name, m_steps=(16, 64, 256)):
             return statistics.median(ts)
         t_round = med(rnd)
         t_evict = med(evict_only)
+        t_round_s = med(rnd_slots)
+        t_evict_s = med(evict_slots_only)
         if nacl.health(ws)[1]:
             raise RuntimeError("a kernel reported a health bit during the generation rounds")
         print(json.dumps({"metric": "generation-phase re-eviction round", "workload": name, "B": w.B, "H": w.H,
                           "D": w.D, "dtype": w.dtype, "C": w.C, "Cr": Cr, "m": m, "cache_rows": L,
                           "round_us": round(t_round, 2), "evict_in_place_us": round(t_evict, 2),
                           "append_us": round(t_round - t_evict, 2),
-                          "us_per_decoding_step": round(t_round / m, 3)}), flush=True)
-        del kc, vc, k_new, v_new, F, keep, ws
+                          "us_per_decoding_step": round(t_round / m, 3),
+                          "slot_form": {"round_us": round(t_round_s, 2), "evict_us": round(t_evict_s, 2),
+                                        "us_per_decoding_step": round(t_round_s / m, 3)}}), flush=True)
+        del kc, vc, k_new, v_new, F, keep, slots, ws
         torch.cuda.empty_cache()
 
 

@@ -151,6 +151,21 @@ int nacl_compact(const nacl_problem* p, const void* k, const void* v,
                  const int32_t* keep_idx, int32_t C, void* k_out, void* v_out,
                  void* stream);
 
+/* Slot form of the in-place cache update, for a generation-phase cache whose
+ * rows need not stay in token order (Section 3, "Generation Phase Eviction":
+ * the paper fixes which entries stay, not where they sit).  keep_idx: device
+ * int32 [B,H,C], the ascending keep set as nacl_select writes it (read only).
+ * In each head of k, v (device [B,H,L,D] with the problem's strides, K and V
+ * disjoint) the kept rows below C stay where they are and the kept rows at or
+ * past C move, in ascending order, into the slots below C whose rows were
+ * not kept (taken in ascending order); nothing else is written, so only the
+ * kept rows past C are copied.  slot_idx: device int32 [B,H,C] (overlapping
+ * nothing above) receives, for each slot c < C, the old row it holds
+ * afterwards.  A keep list that is not an ascending set of rows in [0, L)
+ * gives zero rows in the slots whose mover lies outside [C, L).  Bit copies. */
+int nacl_compact_slots(const nacl_problem* p, void* k, void* v, const int32_t* keep_idx, int32_t C,
+                       int32_t* slot_idx, void* stream);
+
 /* Append of decode steps to the cache (Algorithm 1, generation phase: the
  * new token's key and value join the cache): rows [row0, row0 + m) of every
  * head of k, v (device [B,H,L,D] with the problem's k/v strides) take the m
@@ -177,6 +192,19 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
                int32_t C, int32_t Cr, int32_t sampling, uint64_t seed, uint32_t layer,
                float* scores, int32_t* keep_idx, void* k_out, void* v_out,
                void* ws, size_t ws_bytes, void* stream);
+
+/* Generation-phase eviction with the slot form of the cache update
+ * (Section 3, "Generation Phase Eviction"; the Generation function of
+ * Algorithm 1): nacl_score, nacl_select and nacl_compact_slots on one stream,
+ * in place in k, v.  Arguments as nacl_evict; keep_idx receives the
+ * ascending keep set and slot_idx (device int32 [B,H,C]) the old row each
+ * slot below C holds afterwards.  At decode shapes (L = C + m, the current
+ * token as the only, protected, proxy) only the kept rows among the m newest
+ * move, instead of nearly every kept row as in nacl_evict's in-place form.
+ * The health words of nacl_score apply. */
+int nacl_evict_slots(const nacl_problem* p, const void* q, void* k, void* v, int32_t C, int32_t Cr,
+                     int32_t sampling, uint64_t seed, uint32_t layer, float* scores, int32_t* keep_idx,
+                     int32_t* slot_idx, void* ws, size_t ws_bytes, void* stream);
 
 /* The whole step without a caller workspace, for callers that cannot
  * allocate device memory (code under HIP graph capture, serving loops,

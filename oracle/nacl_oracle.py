@@ -220,6 +220,27 @@ def compact(K, V, keep_idx):
     return K[bi, hi, idx], V[bi, hi, idx]
 
 
+def slot_layout(keep, C):
+    """Where the kept rows of one head sit after a generation-phase eviction
+    that leaves kept rows in place (Section 3, "Generation Phase Eviction";
+    the paper fixes which entries stay, not their order in the cache): a kept
+    row below C keeps its slot; the kept rows at or past C go, in ascending
+    order, to the slots below C whose rows were not kept, also taken in
+    ascending order.  keep: the ascending keep set (C rows).  Returns slot_src
+    with slot_src[c] = the row slot c holds afterwards."""
+    keep = [int(r) for r in keep]
+    assert len(keep) == C and keep == sorted(set(keep))
+    staying = [r for r in keep if r < C]
+    movers = [r for r in keep if r >= C]
+    taken = set(staying)
+    free = [c for c in range(C) if c not in taken]
+    assert len(free) == len(movers)
+    slot_src = list(range(C))
+    for c, r in zip(free, movers):
+        slot_src[c] = r
+    return np.array(slot_src, dtype=np.int64)
+
+
 def evict(Q, K, V, proxy_pos, n_protect, C, Cr, sampling, seed, layer, sm_scale):
     """The whole step for one layer: score, select, compact."""
     F, lse = proxy_scores(Q, K, proxy_pos, sm_scale)

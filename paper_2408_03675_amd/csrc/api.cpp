@@ -390,6 +390,53 @@ int run_compact(const nacl_problem* p, const void* k, const void* v, const int32
   return NACL_OK;
 }
 
+// The slot form's arguments: an in-place update of k, v with keep_idx read
+// and slot_idx written, neither overlapping the caches or each other.
+int check_slots_args(const nacl_problem* p, const void* k, const void* v, const int32_t* keep,
+                     int32_t C, const int32_t* slots) {
+  if (C < 0 || C > p->L) return fail(NACL_ERR_INVALID_ARG, "C must lie in [0, L] (got %d)", C);
+  if (C == 0) return NACL_OK;
+  if (!k || !v || !keep || !slots) return fail(NACL_ERR_INVALID_ARG, "slot-form pointers must be non-NULL");
+  if (!aligned16(k) || !aligned16(v)) return fail(NACL_ERR_INVALID_ARG, "K and V must be 16-byte aligned");
+  uintptr_t k0, k1, v0, v1;
+  extent(k, p->k_stride, p, k0, k1);
+  extent(v, p->v_stride, p, v0, v1);
+  const uintptr_t n = (uintptr_t)p->B * p->H * C * 4;
+  const uintptr_t a0 = (uintptr_t)keep, s0 = (uintptr_t)slots;
+  if (overlaps(k0, k1, v0, v1)) return fail(NACL_ERR_INVALID_ARG, "the slot form needs K and V in disjoint memory");
+  if (overlaps(a0, a0 + n, k0, k1) || overlaps(a0, a0 + n, v0, v1) || overlaps(s0, s0 + n, k0, k1) ||
+      overlaps(s0, s0 + n, v0, v1) || overlaps(a0, a0 + n, s0, s0 + n))
+    return fail(NACL_ERR_INVALID_ARG, "keep_idx / slot_idx overlap K, V or each other");
+  return NACL_OK;
+}
+
+int run_compact_slots(const nacl_problem* p, void* k, void* v, const int32_t* keep, int32_t C, int32_t* slots,
+                      uint32_t* health, hipStream_t stream) {
+  if (C == 0) return NACL_OK;
+  nacl::CompactLaunch c{};
+  const int eb = elt_bytes(p->dtype);
+  c.B = p->B;
+  c.H = p->H;
+  c.L = p->L;
+  c.C = C;
+  c.row_vecs = p->D * eb / 16;
+  for (int i = 0; i < 3; ++i) {
+    c.ks[i] = p->k_stride[i] * eb / 16;
+    c.vs[i] = p->v_stride[i] * eb / 16;
+  }
+  c.k = k;
+  c.v = v;
+  c.keep = keep;
+  c.k_out = k;
+  c.v_out = v;
+  c.in_place = 1;
+  c.health = health;
+  c.slots = slots;
+  hipError_t e = nacl::launch_compact_slots(c, stream);
+  if (e != hipSuccess) return hip_fail(e, "slot-form compact kernel");
+  return NACL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -440,6 +487,15 @@ int nacl_compact(const nacl_problem* p, const void* k, const void* v, const int3
   bool in_place = false;
   if ((st = check_compact_args(p, k, v, keep_idx, C, k_out, v_out, &in_place))) return st;
   return run_compact(p, k, v, keep_idx, C, k_out, v_out, in_place, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int nacl_compact_slots(const nacl_problem* p, void* k, void* v, const int32_t* keep_idx, int32_t C,
+                       int32_t* slot_idx, void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if ((st = check_slots_args(p, k, v, keep_idx, C, slot_idx))) return st;
+  return run_compact_slots(p, k, v, keep_idx, C, slot_idx, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int nacl_append(const nacl_problem* p, void* k, void* v, int32_t row0, const void* k_new,
@@ -513,6 +569,34 @@ int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* 
   if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s, kd.on, true))) return st;
   uint32_t* health = reinterpret_cast<uint32_t*>(w + l.cnt) + 1;
   return run_compact(p, k, v, keep_idx, C, k_out, v_out, in_place, health, s);
+}
+
+int nacl_evict_slots(const nacl_problem* p, const void* q, void* k, void* v, int32_t C, int32_t Cr,
+                     int32_t sampling, uint64_t seed, uint32_t layer, float* scores, int32_t* keep_idx,
+                     int32_t* slot_idx, void* ws, size_t ws_bytes, void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if ((st = check_select_counts(p, C, Cr, sampling))) return st;
+  if (!q || !scores) return fail(NACL_ERR_INVALID_ARG, "q and scores must be non-NULL");
+  if (!aligned16(q)) return fail(NACL_ERR_INVALID_ARG, "q must be 16-byte aligned");
+  if ((st = check_slots_args(p, k, v, keep_idx, C, slot_idx))) return st;
+  if (!k) return fail(NACL_ERR_INVALID_ARG, "k must be non-NULL");
+  if ((st = check_ws(p, ws, ws_bytes))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const Layout l = layout_of(p);
+  char* w = static_cast<char*>(ws);
+  const int* pos_dev = nullptr;
+  if ((st = stage_positions(p, w, l, s, &pos_dev))) return st;
+  KeyDraw kd;
+  kd.on = C > 0 && Cr > 0;
+  kd.sampling = sampling;
+  kd.seed = seed;
+  kd.layer = layer;
+  if ((st = run_score(p, q, k, nullptr, scores, w, l, pos_dev, s, kd))) return st;
+  if ((st = run_select(p, scores, C, Cr, sampling, seed, layer, keep_idx, w, l, pos_dev, s, kd.on, true))) return st;
+  uint32_t* health = reinterpret_cast<uint32_t*>(w + l.cnt) + 1;
+  return run_compact_slots(p, k, v, keep_idx, C, slot_idx, health, s);
 }
 
 const char* nacl_status_string(int status) {

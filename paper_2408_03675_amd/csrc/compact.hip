@@ -102,6 +102,65 @@ __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(Compac
   }
 }
 
+// Slot form of the in-place update (generation-phase eviction with a cache
+// whose rows need not stay in token order): with S the ascending keep set of
+// a head, the kept rows below C stay in their slots, and the kept rows at or
+// past C (the movers, S[n_low..C)) fill the other slots below C (the free
+// slots), both in ascending order.  Only the movers' rows are copied; their
+// sources lie at or past C and their destinations below C, so no copy reads
+// a row another one writes.  slots[c] = the old row slot c holds afterwards.
+// Free slot number fi is f = fi + i*, i* the first i < n_low with
+// S[i] - i > fi (S[i] - i free slots lie below S[i], a non-decreasing count),
+// found by a binary search over S.  One work-group per head; VPR lanes per
+// moved row (K and V).  A mover outside [C, L) (a keep list that is not an
+// ascending set of rows) gives zero rows and sets bit 2 of the health words.
+constexpr int kSlotThreads = 1024;
+
+template <int VPR>
+__global__ __launch_bounds__(kSlotThreads) void compact_slots_kernel(CompactLaunch a) {
+  __shared__ int n_low_s;
+  const int bh = blockIdx.x, b = bh / a.H, h = bh % a.H;
+  const int32_t* S = a.keep + (int64_t)bh * a.C;
+  int32_t* Y = a.slots + (int64_t)bh * a.C;
+  if (threadIdx.x == 0) n_low_s = a.C;
+  __syncthreads();
+  // The first entry at or past C (one writer when S ascends).
+  for (int i = threadIdx.x; i < a.C; i += kSlotThreads)
+    if (S[i] >= a.C && (i == 0 || S[i - 1] < a.C)) n_low_s = i;
+  __syncthreads();
+  const int n_low = n_low_s, n_move = a.C - n_low;
+  for (int i = threadIdx.x; i < n_low; i += kSlotThreads) {
+    const int r = S[i];
+    if ((unsigned)r < (unsigned)a.C) Y[r] = r;  // a kept row below C keeps its slot
+  }
+  u32x4* kb = static_cast<u32x4*>(a.k_out) + b * a.ks[0] + h * a.ks[1];
+  u32x4* vb = static_cast<u32x4*>(a.v_out) + b * a.vs[0] + h * a.vs[1];
+  constexpr int kRowsPerPass = kSlotThreads / VPR;
+  const int vec = threadIdx.x % VPR;
+  for (int fi0 = 0; fi0 < n_move; fi0 += kRowsPerPass) {
+    const int fi = fi0 + (int)threadIdx.x / VPR;
+    if (fi >= n_move) continue;
+    int lo = 0, hi = n_low;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (S[mid] - mid > fi) hi = mid;
+      else lo = mid + 1;
+    }
+    const int f = fi + lo;           // < n_move + n_low = C
+    const int r = S[n_low + fi];     // the mover
+    const bool ok = r >= a.C && r < a.L;
+    if (vec == 0) {
+      Y[f] = r;
+      if (!ok) flag_bad_index(a.health);
+    }
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    const u32x4 xk = ok ? kb[(int64_t)r * a.ks[2] + vec] : z;
+    const u32x4 xv = ok ? vb[(int64_t)r * a.vs[2] + vec] : z;
+    kb[(int64_t)f * a.ks[2] + vec] = xk;
+    vb[(int64_t)f * a.vs[2] + vec] = xv;
+  }
+}
+
 // Append: rows [row0, row0 + m) of every head of the cache take the m rows
 // of k_new / v_new ([B, H, m, D] contiguous).
 __global__ __launch_bounds__(kCompactThreads) void append_kernel(AppendLaunch a) {
@@ -141,6 +200,18 @@ hipError_t launch_compact(const CompactLaunch& a, hipStream_t stream) {
     case 32: return launch_compact_t<32>(a, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_compact_slots(const CompactLaunch& a, hipStream_t stream) {
+  if (a.C == 0) return hipSuccess;
+  if (!a.slots || a.k_out != a.k || a.v_out != a.v) return hipErrorInvalidValue;
+  switch (a.row_vecs) {
+    case 8: hipLaunchKernelGGL(compact_slots_kernel<8>, dim3(a.B * a.H), dim3(kSlotThreads), 0, stream, a); break;
+    case 16: hipLaunchKernelGGL(compact_slots_kernel<16>, dim3(a.B * a.H), dim3(kSlotThreads), 0, stream, a); break;
+    case 32: hipLaunchKernelGGL(compact_slots_kernel<32>, dim3(a.B * a.H), dim3(kSlotThreads), 0, stream, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_append(const AppendLaunch& a, hipStream_t stream) {

@@ -169,9 +169,13 @@ struct CompactLaunch {
   void* v_out;                  // == v when in_place
   int in_place;                 // 1: rows 0..C-1 of each head of k, v take the kept rows
   uint32_t* health;             // health words (call's, sticky) or nullptr
+  int32_t* slots;               // slot form (k_out == k): [B*H, C] old row held by each slot, written
 };
 
 hipError_t launch_compact(const CompactLaunch& L, hipStream_t stream);
+// Slot form of the in-place update: kept rows below C stay, the kept rows at
+// or past C fill the other slots below C (see compact.hip).
+hipError_t launch_compact_slots(const CompactLaunch& L, hipStream_t stream);
 
 struct AppendLaunch {
   int B, H, row0, m, row_vecs;

@@ -27,9 +27,9 @@ SAMPLE_SOFTMAX = 0
 SAMPLE_PROPORTIONAL = 1
 SAMPLE_UNIFORM = 2
 
-EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_append",
-            "nacl_evict", "nacl_evict_noalloc", "nacl_status_string", "nacl_last_error_detail",
-            "nacl_version")
+EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_compact_slots",
+            "nacl_append", "nacl_evict", "nacl_evict_slots", "nacl_evict_noalloc", "nacl_status_string",
+            "nacl_last_error_detail", "nacl_version")
 
 
 class NaclError(RuntimeError):
@@ -73,6 +73,10 @@ def load_library(path=LIB_PATH):
     lib.nacl_select.restype = ctypes.c_int
     lib.nacl_compact.argtypes = [P, vp, vp, vp, i32, vp, vp, vp]
     lib.nacl_compact.restype = ctypes.c_int
+    lib.nacl_compact_slots.argtypes = [P, vp, vp, vp, i32, vp, vp]
+    lib.nacl_compact_slots.restype = ctypes.c_int
+    lib.nacl_evict_slots.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, sz, vp]
+    lib.nacl_evict_slots.restype = ctypes.c_int
     lib.nacl_append.argtypes = [P, vp, vp, i32, vp, vp, i32, vp]
     lib.nacl_append.restype = ctypes.c_int
     lib.nacl_evict.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, vp, sz, vp]
@@ -276,6 +280,25 @@ def compact(prob, k, v, keep_idx, k_out=None, v_out=None, in_place=False):
     return k_out, v_out
 
 
+def compact_slots(prob, k, v, keep_idx, slot_idx=None):
+    """Slot form of the in-place cache update (Section 3, generation phase):
+    kept rows below C stay, kept rows at or past C fill the other slots below
+    C, in ascending order.  keep_idx [B, H, C] is the ascending keep set.
+    Returns slot_idx [B, H, C]: the old row each slot holds afterwards."""
+    lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    prob.qkv(k, "k", dev, "k")
+    prob.qkv(v, "v", dev, "v")
+    C = keep_idx.shape[-1]
+    _gpu(keep_idx, "keep_idx", dev, (prob.B, prob.H, C), torch.int32, contiguous=True)
+    if slot_idx is None:
+        slot_idx = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=dev)
+    _gpu(slot_idx, "slot_idx", dev, (prob.B, prob.H, C), torch.int32, contiguous=True)
+    _check(lib.nacl_compact_slots(prob.ref(), _ptr(k), _ptr(v), _ptr(keep_idx), int(C), _ptr(slot_idx),
+                                  _stream(k.device)))
+    return slot_idx
+
+
 def append(prob, k, v, row0, k_new, v_new):
     """Rows [row0, row0 + m) of every head of the cache k, v take k_new, v_new
     [B, H, m, D] (Algorithm 1, generation phase)."""
@@ -321,6 +344,34 @@ def evict(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=Non
                           int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(k_out),
                           _ptr(v_out), _ptr(ws), ws.numel(), _stream(dev)))
     return scores, keep_idx, k_out, v_out
+
+
+def evict_slots(prob, q, k, v, C, Cr, sampling=SAMPLE_SOFTMAX, seed=0, layer=0, ws=None,
+                scores=None, keep_idx=None, slot_idx=None):
+    """score -> select -> slot-form in-place update of k, v on the current
+    stream (generation-phase eviction, Section 3).  Returns (scores, keep_idx,
+    slot_idx): the ascending keep set and the old row each slot below C
+    holds afterwards."""
+    lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    for t, name in ((q, "q"), (k, "k"), (v, "v")):
+        prob.qkv(t, name, dev, name)
+    if ws is None:
+        ws = workspace(prob, dev)
+    if scores is None:
+        scores = torch.empty((prob.B, prob.H, prob.L), dtype=torch.float32, device=dev)
+    if keep_idx is None:
+        keep_idx = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=dev)
+    if slot_idx is None:
+        slot_idx = torch.empty((prob.B, prob.H, C), dtype=torch.int32, device=dev)
+    _gpu(ws, "ws", dev, dtype=torch.uint8, contiguous=True)
+    _gpu(scores, "scores", dev, (prob.B, prob.H, prob.L), torch.float32, contiguous=True)
+    for t, name in ((keep_idx, "keep_idx"), (slot_idx, "slot_idx")):
+        _gpu(t, name, dev, (prob.B, prob.H, int(C)), torch.int32, contiguous=True)
+    _check(lib.nacl_evict_slots(prob.ref(), _ptr(q), _ptr(k), _ptr(v), int(C), int(Cr), int(sampling),
+                                int(seed), int(layer), _ptr(scores), _ptr(keep_idx), _ptr(slot_idx),
+                                _ptr(ws), ws.numel(), _stream(dev)))
+    return scores, keep_idx, slot_idx
 
 
 NOALLOC_WORKSPACE_MAX = 64 << 20

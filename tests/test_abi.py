@@ -133,6 +133,36 @@ def test_in_place_compaction_checks(lib):
     assert st == nacl.NACL_ERR_INVALID_ARG
 
 
+def test_slot_form_checks(lib):
+    """The slot form of the in-place update needs K and V disjoint and
+    keep_idx / slot_idx outside both caches and each other; C must lie in
+    [0, L]; anything else is refused before a launch (nacl_compact_slots and
+    nacl_evict_slots alike)."""
+    p = _prob()
+    k = 1 << 30
+    kbytes = 2 * 4 * 1000 * 128 * 2
+    K, V, KEEP, SLOTS = (ctypes.c_void_p(x) for x in (k, k + 2 * kbytes, k + 8 * kbytes, k + 9 * kbytes))
+    # K and V overlap
+    st = lib.nacl_compact_slots(p.ref(), K, ctypes.c_void_p(k + 4096), KEEP, 200, SLOTS, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # slot_idx inside V
+    st = lib.nacl_compact_slots(p.ref(), K, V, KEEP, 200, ctypes.c_void_p(k + 2 * kbytes + 512), None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # slot_idx overlapping keep_idx
+    st = lib.nacl_compact_slots(p.ref(), K, V, KEEP, 200, ctypes.c_void_p(k + 8 * kbytes + 64), None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # C past L, and a missing slot_idx
+    st = lib.nacl_compact_slots(p.ref(), K, V, KEEP, 1001, SLOTS, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    st = lib.nacl_compact_slots(p.ref(), K, V, KEEP, 200, None, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+    # the whole step: the same overlap rule before any launch
+    Q = ctypes.c_void_p(k + 16 * kbytes)
+    F = ctypes.c_void_p(k + 20 * kbytes)
+    st = lib.nacl_evict_slots(p.ref(), Q, K, V, 200, 100, 0, 1, 0, F, KEEP, ctypes.c_void_p(k + 64), None, 0, None)
+    assert st == nacl.NACL_ERR_INVALID_ARG
+
+
 @pytest.mark.parametrize("row0,m", [(-1, 4), (990, 11), (0, -1)])
 def test_append_range_checks(lib, row0, m):
     p = _prob()
