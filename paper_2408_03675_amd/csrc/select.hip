@@ -160,9 +160,13 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scan_buf) {
 
 constexpr int kRegKeys = 32;
 constexpr int kRegMaxL = kRegKeys * kSelThreads;
+// Heads of up to 32 * kSelSmallThreads tokens take a work-group of that
+// many threads: the same steps with a quarter of the waves per barrier.
+constexpr int kSelSmallThreads = 256;
 static_assert(kRegMaxL == kSelRegMaxL, "register selection length");
 constexpr int kHistBins = 4096;
 static_assert(kHistBins == 64 * kWave, "histogram scan: 64 bins per lane of one wave");
+static_assert(kHistBins % kSelSmallThreads == 0, "histogram clears");
 constexpr int kRegCand = kWave;  // bins resolved by one wave
 
 // A barrier without the full fence of __syncthreads(): it waits for this
@@ -203,12 +207,15 @@ __device__ __forceinline__ uint32_t lds_add_rtn(uint32_t* p, uint32_t v) {
   return r;
 }
 
+// LDS of a work-group of NT threads.
+template <int NT>
 struct RegLds {
+  static constexpr int kWaves = NT / kWave;
   alignas(16) uint32_t hist[kHistBins];  // all zero between passes
-  uint32_t fixed[kRegMaxL / 32];         // Pi, one bit per token (word t: tokens 32 t ..)
+  uint32_t fixed[NT];                    // Pi, one bit per token (word t: tokens 32 t ..)
   uint32_t cand[kRegCand];               // keys of the k-th bin (step 3)
   uint32_t pick[2][4];                   // per rank: found, bin, rank within the bin, bin count
-  uint32_t scan[2 * kSelWaves];
+  uint32_t scan[2 * kWaves];
   uint32_t shv[8];                       // 0-2 ranked result, 4 gather counter, 5 max key, 6 valid samples
 };
 
@@ -233,18 +240,19 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t x) {
 // Exclusive prefix sum of v over the work-group in thread order (the scan of
 // block_exclusive_scan with barriers that leave the buffer->LDS loads in
 // flight).
+template <int NW>
 __device__ __forceinline__ uint32_t reg_block_scan(uint32_t v, uint32_t* scan_buf) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t x = wave_inclusive_scan(v);
   if (lane == kWave - 1) scan_buf[wave] = x;
   lds_barrier();
   if (wave == 0) {
-    uint32_t t = lane < kSelWaves ? scan_buf[lane] : 0u;
+    uint32_t t = lane < NW ? scan_buf[lane] : 0u;
     t = wave_inclusive_scan(t);
-    if (lane < kSelWaves) scan_buf[kSelWaves + lane] = t;
+    if (lane < NW) scan_buf[NW + lane] = t;
   }
   lds_barrier();
-  const uint32_t base = wave ? scan_buf[kSelWaves + wave - 1] : 0u;
+  const uint32_t base = wave ? scan_buf[NW + wave - 1] : 0u;
   return base + x - v;
 }
 
@@ -328,8 +336,8 @@ __device__ __forceinline__ void pick_bins(uint32_t* hist, uint32_t (*pick)[4], c
   lds_barrier();
 }
 
-template <int NRK>
-__device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) {
+template <int NRK, class Lds>
+__device__ __forceinline__ void pick_bins(Lds& s, const uint32_t (&kr)[NRK]) {
   pick_bins(s.hist, s.pick, kr);
 }
 
@@ -337,8 +345,8 @@ __device__ __forceinline__ void pick_bins(RegLds& s, const uint32_t (&kr)[NRK]) 
 // of prefix (its lower bits zero; bits == 32: every key), by radix passes of
 // 12 bits (the last one narrower) over the bits below; key 0 never counts.
 // At least kr keys must match.
-template <int NR>
-__device__ __forceinline__ TopK radix_rest(const uint32_t (&key)[NR], RegLds& s, uint32_t prefix, int bits,
+template <int NR, class Lds>
+__device__ __forceinline__ TopK radix_rest(const uint32_t (&key)[NR], Lds& s, uint32_t prefix, int bits,
                                            uint32_t kr) {
   uint32_t n_eq = 0u;
 #pragma unroll 1
@@ -363,8 +371,8 @@ __device__ __forceinline__ TopK radix_rest(const uint32_t (&key)[NR], RegLds& s,
 
 // Top k (1 <= k <= number of nonzero keys) of the register keys; n_valid is
 // the number of nonzero keys of the head (it only scales the sample ranks).
-template <int NR>
-__device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k, uint32_t n_valid, RegLds& s) {
+template <int NR, class Lds>
+__device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k, uint32_t n_valid, Lds& s) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // 1. One sampled key per thread (slot 0, whose token offset rotates from
   // thread to thread), and the largest key.
@@ -459,9 +467,9 @@ __device__ __forceinline__ TopK reg_top_k(const uint32_t (&key)[NR], uint32_t k,
 
 // Bit i: the token of slot i belongs to the top k described by r (rot: the
 // thread's slot rotation).
-template <int NR>
+template <int NR, class Lds>
 __device__ __forceinline__ uint32_t top_members(const uint32_t (&key)[NR], const TopK& r, uint32_t rot,
-                                                RegLds& s) {
+                                                Lds& s) {
   uint32_t in = 0u;
   if (r.need == r.n_eq) {
 #pragma unroll
@@ -477,7 +485,7 @@ __device__ __forceinline__ uint32_t top_members(const uint32_t (&key)[NR], const
   }
   uint32_t t_tok = rotl32(tie, rot);  // token order
   const uint32_t n = (uint32_t)__popc(t_tok);
-  const uint32_t before = reg_block_scan(n, s.scan);
+  const uint32_t before = reg_block_scan<Lds::kWaves>(n, s.scan);
   uint32_t take = min(r.need - min(r.need, before), n);  // need - before, or 0 past the need-th tie
   uint32_t kept_tok = 0u;
   while (take--) {
@@ -488,9 +496,12 @@ __device__ __forceinline__ uint32_t top_members(const uint32_t (&key)[NR], const
   return in | rotr32(kept_tok, rot);
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a) {
-  __shared__ RegLds s;
-  __shared__ uint32_t stage[kRegMaxL];  // one key set of the head, by buffer->LDS loads
+template <int NT>
+__global__ __launch_bounds__(NT) void select_kernel_regs(SelectLaunch a) {
+  constexpr int kNW = NT / kWave;          // waves
+  constexpr int kMaxL = kRegKeys * NT;     // tokens the work-group holds
+  __shared__ RegLds<NT> s;
+  __shared__ uint32_t stage[kMaxL];  // one key set of the head, by buffer->LDS loads
   const int L = a.L;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int bh = blockIdx.x;
@@ -508,15 +519,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
         const_cast<uint32_t*>(src), (short)0, (int)((uint32_t)n * 4u), kSelBufferRsrcWord3);
     if ((L & 3) == 0 && ((uintptr_t)src & 15u) == 0) {
 #pragma unroll
-      for (int r = 0; r < kRegMaxL / (256 * kSelWaves); ++r) {
-        const uint32_t t0 = 256u * (uint32_t)(kSelWaves * r + wave);
+      for (int r = 0; r < kMaxL / (256 * kNW); ++r) {
+        const uint32_t t0 = 256u * (uint32_t)(kNW * r + wave);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + t0), 16,
                                                  (t0 + 4u * (uint32_t)lane) * 4u, 0, 0, 0);
       }
     } else {
 #pragma unroll
-      for (int r = 0; r < kRegMaxL / (64 * kSelWaves); ++r) {
-        const uint32_t t0 = 64u * (uint32_t)(kSelWaves * r + wave);
+      for (int r = 0; r < kMaxL / (64 * kNW); ++r) {
+        const uint32_t t0 = 64u * (uint32_t)(kNW * r + wave);
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(stage + t0), 4,
                                                  (t0 + (uint32_t)lane) * 4u, 0, 0, 0);
       }
@@ -540,12 +551,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
   stage_keys(fsrc, a.Cp > 0 ? L : 0);
   s.fixed[tid] = 0u;
 #pragma unroll
-  for (int q = 0; q < kHistBins / kSelThreads; ++q) s.hist[q * kSelThreads + tid] = 0u;
+  for (int q = 0; q < kHistBins / NT; ++q) s.hist[q * NT + tid] = 0u;
   if (tid < 8) s.shv[tid] = 0u;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's loads
   lds_barrier();                                    // everyone's, and the clears
   if (p0 >= 0) lds_or(&s.fixed[p0 >> 5], 1u << (p0 & 31));
-  for (int i = pbase + tid + kSelThreads; i < a.P; i += kSelThreads) {
+  for (int i = pbase + tid + NT; i < a.P; i += NT) {
     const int j = a.pos[i];
     lds_or(&s.fixed[j >> 5], 1u << (j & 31));
   }
@@ -592,7 +603,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
   // selection's barriers), then copied out with coalesced stores.
   uint32_t kept = rotl32(mp | ms | mr, rot);
   if (a.Cr == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the zero loads into the buffer
-  uint32_t o = reg_block_scan((uint32_t)__popc(kept), s.scan);  // (its barriers: everyone's)
+  uint32_t o = reg_block_scan<kNW>((uint32_t)__popc(kept), s.scan);  // (its barriers: everyone's)
   while (kept) {
     const int b = __builtin_ctz(kept);
     if (o < (uint32_t)a.C) stage[o] = (uint32_t)(kRegKeys * tid + b);
@@ -601,7 +612,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel_regs(SelectLaunch a
   }
   lds_barrier();
   int32_t* out = a.keep + (int64_t)bh * a.C;
-  for (int c = tid; c < a.C; c += kSelThreads) out[c] = (int32_t)stage[c];
+  for (int c = tid; c < a.C; c += NT) out[c] = (int32_t)stage[c];
 }
 
 // ===========================================================================
@@ -1124,8 +1135,12 @@ hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  if (a.L <= kRegKeys * kSelSmallThreads) {
+    hipLaunchKernelGGL(select_kernel_regs<kSelSmallThreads>, dim3(BH), dim3(kSelSmallThreads), 0, stream, a);
+    return hipGetLastError();
+  }
   if (a.L <= kRegMaxL) {
-    hipLaunchKernelGGL(select_kernel_regs, dim3(BH), dim3(kSelThreads), 0, stream, a);
+    hipLaunchKernelGGL(select_kernel_regs<kSelThreads>, dim3(BH), dim3(kSelThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.nb < 1 || a.nb > kSelMaxSlices || (int64_t)a.nb * kSelSlice < a.L) return hipErrorInvalidValue;
