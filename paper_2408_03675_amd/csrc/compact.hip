@@ -115,49 +115,63 @@ __global__ __launch_bounds__(kInplaceThreads) void compact_inplace_kernel(Compac
 // moved row (K and V).  A mover outside [C, L) (a keep list that is not an
 // ascending set of rows) gives zero rows and sets bit 2 of the health words.
 constexpr int kSlotThreads = 1024;
+constexpr int kSlotLdsKeep = 16384;  // keep lists up to this long are searched in LDS
 
 template <int VPR>
 __global__ __launch_bounds__(kSlotThreads) void compact_slots_kernel(CompactLaunch a) {
   __shared__ int n_low_s;
+  __shared__ int32_t keep_lds[kSlotLdsKeep];
   const int bh = blockIdx.x, b = bh / a.H, h = bh % a.H;
-  const int32_t* S = a.keep + (int64_t)bh * a.C;
+  const int32_t* Sg = a.keep + (int64_t)bh * a.C;
   int32_t* Y = a.slots + (int64_t)bh * a.C;
-  if (threadIdx.x == 0) n_low_s = a.C;
-  __syncthreads();
-  // The first entry at or past C (one writer when S ascends).
-  for (int i = threadIdx.x; i < a.C; i += kSlotThreads)
-    if (S[i] >= a.C && (i == 0 || S[i - 1] < a.C)) n_low_s = i;
-  __syncthreads();
-  const int n_low = n_low_s, n_move = a.C - n_low;
-  for (int i = threadIdx.x; i < n_low; i += kSlotThreads) {
-    const int r = S[i];
-    if ((unsigned)r < (unsigned)a.C) Y[r] = r;  // a kept row below C keeps its slot
-  }
   u32x4* kb = static_cast<u32x4*>(a.k_out) + b * a.ks[0] + h * a.ks[1];
   u32x4* vb = static_cast<u32x4*>(a.v_out) + b * a.vs[0] + h * a.vs[1];
   constexpr int kRowsPerPass = kSlotThreads / VPR;
   const int vec = threadIdx.x % VPR;
-  for (int fi0 = 0; fi0 < n_move; fi0 += kRowsPerPass) {
-    const int fi = fi0 + (int)threadIdx.x / VPR;
-    if (fi >= n_move) continue;
-    int lo = 0, hi = n_low;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (S[mid] - mid > fi) hi = mid;
-      else lo = mid + 1;
+  // The steps, over the keep list S (called with the LDS copy or with the
+  // list in memory, each call on a pointer whose memory the compiler knows:
+  // no generic pointer into LDS is formed).
+  auto run = [&](const int32_t* S) {
+    if (threadIdx.x == 0) n_low_s = a.C;
+    __syncthreads();
+    // The first entry at or past C (one writer when S ascends).
+    for (int i = threadIdx.x; i < a.C; i += kSlotThreads)
+      if (S[i] >= a.C && (i == 0 || S[i - 1] < a.C)) n_low_s = i;
+    __syncthreads();
+    const int n_low = n_low_s, n_move = a.C - n_low;
+    for (int i = threadIdx.x; i < n_low; i += kSlotThreads) {
+      const int r = S[i];
+      if ((unsigned)r < (unsigned)a.C) Y[r] = r;  // a kept row below C keeps its slot
     }
-    const int f = fi + lo;           // < n_move + n_low = C
-    const int r = S[n_low + fi];     // the mover
-    const bool ok = r >= a.C && r < a.L;
-    if (vec == 0) {
-      Y[f] = r;
-      if (!ok) flag_bad_index(a.health);
+    for (int fi0 = 0; fi0 < n_move; fi0 += kRowsPerPass) {
+      const int fi = fi0 + (int)threadIdx.x / VPR;
+      if (fi >= n_move) continue;
+      int lo = 0, hi = n_low;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (S[mid] - mid > fi) hi = mid;
+        else lo = mid + 1;
+      }
+      const int f = fi + lo;           // < n_move + n_low = C
+      const int r = S[n_low + fi];     // the mover
+      const bool ok = r >= a.C && r < a.L;
+      if (vec == 0) {
+        Y[f] = r;
+        if (!ok) flag_bad_index(a.health);
+      }
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      const u32x4 xk = ok ? kb[(int64_t)r * a.ks[2] + vec] : z;
+      const u32x4 xv = ok ? vb[(int64_t)r * a.vs[2] + vec] : z;
+      kb[(int64_t)f * a.ks[2] + vec] = xk;
+      vb[(int64_t)f * a.vs[2] + vec] = xv;
     }
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    const u32x4 xk = ok ? kb[(int64_t)r * a.ks[2] + vec] : z;
-    const u32x4 xv = ok ? vb[(int64_t)r * a.vs[2] + vec] : z;
-    kb[(int64_t)f * a.ks[2] + vec] = xk;
-    vb[(int64_t)f * a.vs[2] + vec] = xv;
+  };
+  // The binary searches read the keep list many times: from LDS when it fits.
+  if (a.C <= kSlotLdsKeep) {
+    for (int i = threadIdx.x; i < a.C; i += kSlotThreads) keep_lds[i] = Sg[i];
+    run(keep_lds);
+  } else {
+    run(Sg);
   }
 }
 
