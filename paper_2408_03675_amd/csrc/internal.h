@@ -103,6 +103,7 @@ struct ScoreSched {
   float* logits;         // few-row path (nullptr otherwise): [B*H, P, logits_stride] raw logits
   int logits_stride;     // L rounded up to a multiple of 4
   int row_pos[16];       // few-row path: position of row r (proxy r / qg), from the host
+  int n_clear;           // few-row path: counter words (from queue) its first work-group zeroes
   const float* lse_in;   // caller's log-sum-exp when lse_given
   float lse_mul;         // log2(e) for a natural log-sum-exp
   float* scores;         // [B*H, L]

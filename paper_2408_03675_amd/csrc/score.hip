@@ -801,6 +801,12 @@ __global__ __launch_bounds__(kScoreThreads) void score_rows_logits_kernel(const 
   const int r16 = lane & 15, g = lane >> 4;
   const int chunk = blockIdx.x, bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
   const int tpw = s.chunk_keys / (16 * kScoreWaves);  // this launch's tiles per wave, 1 .. kTiles
+  // The first work-group zeroes the workspace's counter words (the call's
+  // health word, the selection's synchronisation words), all but the sticky
+  // health word (word 2); nothing in this launch reads them.
+  if (chunk == 0 && bh == 0)
+    for (int i = threadIdx.x; i < s.n_clear; i += kScoreThreads)
+      if (i != 2) s.queue[i] = 0u;
   const int key_c0 = chunk * s.chunk_keys;
   float2* part = s.partials + ((int64_t)bh * s.n_chunks + chunk) * a.P;
   const float c2 = a.c2;
@@ -1537,15 +1543,13 @@ hipError_t launch_score_split(const ScoreLaunch& L, hipStream_t stream) {
 
 template <typename T, int D>
 hipError_t launch_score_rows_t(const ScoreLaunch& L, hipStream_t stream) {
-  const ScoreSched& s = L.sched;
+  ScoreSched s = L.sched;
+  s.n_clear = L.n_counter_words;  // cleared by the logit kernel: no separate clearing launch
   const int BH = L.args.B * L.args.H;
-  const int init_blocks = std::max(1, std::min(64, (L.n_counter_words + 255) / 256));
-  hipLaunchKernelGGL(score_init_kernel, dim3(init_blocks), dim3(256), 0, stream, s.queue, L.n_counter_words);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((score_rows_logits_kernel<T, D>), dim3(s.n_chunks, BH), dim3(kScoreThreads), 0, stream,
                      static_cast<const T*>(L.q), static_cast<const T*>(L.k), L.args, s);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const int col_blocks = (L.args.L + 4 * kScoreThreads - 1) / (4 * kScoreThreads);
   hipLaunchKernelGGL(score_rows_column_kernel, dim3(col_blocks, BH), dim3(kScoreThreads), 0, stream, L.args, s);
   return hipGetLastError();
