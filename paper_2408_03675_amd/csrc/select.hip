@@ -160,13 +160,12 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scan_buf) {
 
 constexpr int kRegKeys = 32;
 constexpr int kRegMaxL = kRegKeys * kSelThreads;
-// Heads of up to 32 * kSelSmallThreads tokens take a work-group of that
-// many threads: the same steps with a quarter of the waves per barrier.
-constexpr int kSelSmallThreads = 256;
+// Shorter heads hold 8 or 16 tokens per thread (up to 8 or 16 times
+// kSelThreads tokens): the same steps with fewer slots per thread.
 static_assert(kRegMaxL == kSelRegMaxL, "register selection length");
 constexpr int kHistBins = 4096;
 static_assert(kHistBins == 64 * kWave, "histogram scan: 64 bins per lane of one wave");
-static_assert(kHistBins % kSelSmallThreads == 0, "histogram clears");
+
 constexpr int kRegCand = kWave;  // bins resolved by one wave
 
 // A barrier without the full fence of __syncthreads(): it waits for this
@@ -225,6 +224,16 @@ struct TopK {
 
 __device__ __forceinline__ uint32_t rotr32(uint32_t x, uint32_t r) { return __builtin_amdgcn_alignbit(x, x, r); }
 __device__ __forceinline__ uint32_t rotl32(uint32_t x, uint32_t r) { return __builtin_amdgcn_alignbit(x, x, (32u - r) & 31u); }
+// Rotations of the low NR bits of a mask (NR slots per thread, r < NR).
+template <int NR>
+__device__ __forceinline__ uint32_t rotr_n(uint32_t x, uint32_t r) {
+  if constexpr (NR == 32) return rotr32(x, r);
+  else return ((x >> r) | (x << ((NR - r) & 31u))) & ((1u << NR) - 1u);
+}
+template <int NR>
+__device__ __forceinline__ uint32_t rotl_n(uint32_t x, uint32_t r) {
+  return rotr_n<NR>(x, (NR - r) % NR);
+}
 
 // Maximum over the wave (the inclusive scan's shifts with max).
 __device__ __forceinline__ uint32_t wave_max(uint32_t x) {
@@ -483,7 +492,7 @@ __device__ __forceinline__ uint32_t top_members(const uint32_t (&key)[NR], const
     in |= (key[i] > r.T ? 1u : 0u) << i;
     tie |= (key[i] == r.T ? 1u : 0u) << i;
   }
-  uint32_t t_tok = rotl32(tie, rot);  // token order
+  uint32_t t_tok = rotl_n<NR>(tie, rot);  // token order
   const uint32_t n = (uint32_t)__popc(t_tok);
   const uint32_t before = reg_block_scan<Lds::kWaves>(n, s.scan);
   uint32_t take = min(r.need - min(r.need, before), n);  // need - before, or 0 past the need-th tie
@@ -493,13 +502,14 @@ __device__ __forceinline__ uint32_t top_members(const uint32_t (&key)[NR], const
     kept_tok |= low;
     t_tok ^= low;
   }
-  return in | rotr32(kept_tok, rot);
+  return in | rotr_n<NR>(kept_tok, rot);
 }
 
-template <int NT>
+template <int NT, int NR>
 __global__ __launch_bounds__(NT) void select_kernel_regs(SelectLaunch a) {
+  static_assert(NR == 8 || NR == 16 || NR == 32, "keys per thread");
   constexpr int kNW = NT / kWave;          // waves
-  constexpr int kMaxL = kRegKeys * NT;     // tokens the work-group holds
+  constexpr int kMaxL = NR * NT;           // tokens the work-group holds
   __shared__ RegLds<NT> s;
   __shared__ uint32_t stage[kMaxL];  // one key set of the head, by buffer->LDS loads
   const int L = a.L;
@@ -533,14 +543,14 @@ __global__ __launch_bounds__(NT) void select_kernel_regs(SelectLaunch a) {
       }
     }
   };
-  // Thread t's 32 staged words, slot i = token 32 t + ((i + rot) mod 32).
-  const uint32_t rot = (4u * (uint32_t)tid) & 31u;
-  uint32_t key[kRegKeys];
+  // Thread t's NR staged words, slot i = token NR t + ((i + rot) mod NR).
+  const uint32_t rot = (4u * (uint32_t)tid) & (uint32_t)(NR - 1);
+  uint32_t key[NR];
   auto read_stage = [&]() {
-    const uint4* row = reinterpret_cast<const uint4*>(stage + kRegKeys * tid);
+    const uint4* row = reinterpret_cast<const uint4*>(stage + NR * tid);
 #pragma unroll
-    for (int q = 0; q < kRegKeys / 4; ++q) {
-      const uint4 v = row[(q + tid) & 7];
+    for (int q = 0; q < NR / 4; ++q) {
+      const uint4 v = row[(q + tid) & (NR / 4 - 1)];
       key[4 * q] = v.x;
       key[4 * q + 1] = v.y;
       key[4 * q + 2] = v.z;
@@ -569,16 +579,19 @@ __global__ __launch_bounds__(NT) void select_kernel_regs(SelectLaunch a) {
 
   // Bit i of each mask: the token of slot i is in Pi (mp), u_score (ms),
   // u_random (mr).  Tokens past the end are in none.
-  const int nt = L - kRegKeys * tid;
-  const uint32_t live_tok = nt >= kRegKeys ? 0xFFFFFFFFu : (nt > 0 ? (1u << nt) - 1u : 0u);
-  const uint32_t live = rotr32(live_tok, rot);
-  const uint32_t mp = rotr32(s.fixed[tid], rot);
+  const int nt = L - NR * tid;
+  const uint32_t all = NR == 32 ? 0xFFFFFFFFu : (1u << NR) - 1u;
+  const uint32_t live_tok = nt >= NR ? all : (nt > 0 ? (1u << nt) - 1u : 0u);
+  const uint32_t live = rotr_n<NR>(live_tok, rot);
+  // This thread's NR bits of the token bitmap (word w: tokens 32 w .. 32 w + 31).
+  const uint32_t fixed_tok = NR == 32 ? s.fixed[tid] : (s.fixed[(NR * tid) >> 5] >> ((NR * tid) & 31)) & all;
+  const uint32_t mp = rotr_n<NR>(fixed_tok, rot);
   uint32_t ms = 0u, mr = 0u;
 
   // u_score: top-Cp of F over R = [0, L) \ Pi.
   if (a.Cp > 0) {
 #pragma unroll
-    for (int i = 0; i < kRegKeys; ++i)
+    for (int i = 0; i < NR; ++i)
       key[i] = ((live & ~mp) >> i) & 1u ? float_order_key(__uint_as_float(key[i])) : 0u;
     const TopK r = reg_top_k(key, (uint32_t)a.Cp, (uint32_t)(L - a.n_protect), s);
     ms = top_members(key, r, rot, s);
@@ -591,7 +604,7 @@ __global__ __launch_bounds__(NT) void select_kernel_regs(SelectLaunch a) {
     read_stage();
     const uint32_t cand = live & ~mp & ~ms;
 #pragma unroll
-    for (int i = 0; i < kRegKeys; ++i)
+    for (int i = 0; i < NR; ++i)
       if (!((cand >> i) & 1u)) key[i] = 0u;
     const TopK r = reg_top_k(key, (uint32_t)a.Cr, (uint32_t)(L - a.n_protect - a.Cp), s);
     mr = top_members(key, r, rot, s);
@@ -601,12 +614,12 @@ __global__ __launch_bounds__(NT) void select_kernel_regs(SelectLaunch a) {
   // (the bound only guards the write).  The list is assembled in the staging
   // buffer (every thread has read the Gumbel keys from it before the last
   // selection's barriers), then copied out with coalesced stores.
-  uint32_t kept = rotl32(mp | ms | mr, rot);
+  uint32_t kept = rotl_n<NR>(mp | ms | mr, rot);
   if (a.Cr == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the zero loads into the buffer
   uint32_t o = reg_block_scan<kNW>((uint32_t)__popc(kept), s.scan);  // (its barriers: everyone's)
   while (kept) {
     const int b = __builtin_ctz(kept);
-    if (o < (uint32_t)a.C) stage[o] = (uint32_t)(kRegKeys * tid + b);
+    if (o < (uint32_t)a.C) stage[o] = (uint32_t)(NR * tid + b);
     ++o;
     kept &= kept - 1u;
   }
@@ -1135,12 +1148,16 @@ hipError_t launch_select(const SelectLaunch& a, hipStream_t stream) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  if (a.L <= kRegKeys * kSelSmallThreads) {
-    hipLaunchKernelGGL(select_kernel_regs<kSelSmallThreads>, dim3(BH), dim3(kSelSmallThreads), 0, stream, a);
+  if (a.L <= 8 * kSelThreads) {
+    hipLaunchKernelGGL((select_kernel_regs<kSelThreads, 8>), dim3(BH), dim3(kSelThreads), 0, stream, a);
+    return hipGetLastError();
+  }
+  if (a.L <= 16 * kSelThreads) {
+    hipLaunchKernelGGL((select_kernel_regs<kSelThreads, 16>), dim3(BH), dim3(kSelThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.L <= kRegMaxL) {
-    hipLaunchKernelGGL(select_kernel_regs<kSelThreads>, dim3(BH), dim3(kSelThreads), 0, stream, a);
+    hipLaunchKernelGGL((select_kernel_regs<kSelThreads, kRegKeys>), dim3(BH), dim3(kSelThreads), 0, stream, a);
     return hipGetLastError();
   }
   if (a.nb < 1 || a.nb > kSelMaxSlices || (int64_t)a.nb * kSelSlice < a.L) return hipErrorInvalidValue;
