@@ -10,7 +10,7 @@
 //
 // Keys are order-preserving uint32 images of the binary32 values (0 marks a
 // token that is not a candidate).  Heads of up to kRegMaxL tokens take one
-// work-group each, every thread holding 32 tokens' keys in registers
+// work-group each, every thread holding up to 32 tokens' keys in registers
 // (select_kernel_regs, described with it below).  Longer heads are cut into
 // slices of kSelSlice tokens, one work-group each, every thread holding
 // kSelPer consecutive tokens in registers; the work-groups of a head exchange
@@ -127,14 +127,17 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* scan_buf) {
 // ===========================================================================
 // Heads of up to kRegMaxL tokens: one work-group per head.
 //
-// Thread t holds the keys of the 32 consecutive tokens 32 t .. 32 t + 31 in
-// registers.  Each key set (scores, then Gumbel keys) is staged in LDS by
-// direct buffer->LDS loads (contiguous 16-byte pieces per lane) and read
-// back as eight 16-byte pieces per thread in the rotated order (q + t) mod 8,
-// under which the eight lanes an LDS cycle serves touch distinct banks; so
-// register slot i holds token 32 t + ((i + 4 t) mod 32), and a mask over the
-// slots is a mask over the thread's tokens rotated by 4 t.  The Gumbel keys
-// are loaded into the staging buffer while the scores are searched.
+// Thread t holds the keys of the NR consecutive tokens NR t .. NR t + NR - 1
+// in registers (NR = 32, or 16 or 8 for heads of at most 16 or 8 times the
+// work-group's threads: fewer slots per thread, the same steps).  Each key
+// set (scores, then Gumbel keys) is staged in LDS by direct buffer->LDS loads
+// (contiguous 16-byte pieces per lane) and read back as NR / 4 16-byte pieces
+// per thread in the rotated order (q + t) mod (NR / 4), which spreads the
+// lanes an LDS cycle serves over the banks (for NR = 32 over distinct ones);
+// so register slot i holds token NR t + ((i + 4 t) mod NR), and a mask over
+// the slots is a mask over the thread's tokens rotated by 4 t mod NR.  The
+// Gumbel keys are loaded into the staging buffer while the scores are
+// searched.
 // Top-k of one key set (the k-th largest key T, and `need`, how many keys
 // equal to T the top k holds; ties go to the lower index):
 //   1. window: one sampled key per thread (a different slot in each thread,
