@@ -101,13 +101,14 @@ def test_score_matches_oracle(case):
     _say("  max rel err", rel)
 
 
-def test_score_strided_inputs():
-    """Q, K, V as [B, H, L, D] views of [B, L, H, D] buffers."""
+@pytest.mark.parametrize("pos", [list(range(650, 700)), [10, 350, 699]], ids=["p50", "few_rows"])
+def test_score_strided_inputs(pos):
+    """Q, K, V as [B, H, L, D] views of [B, L, H, D] buffers (50 proxies, and
+    three: the few-row path)."""
     B, H, L, D = 2, 4, 700, 128
     g = torch.Generator(device="cuda").manual_seed(7)
     base = torch.randn((3, B, L, H, D), generator=g, device="cuda").to(torch.bfloat16)
     q, k, v = (base[i].permute(0, 2, 1, 3) for i in range(3))
-    pos = list(range(650, 700))
     prob = nacl.Problem.from_tensors(q, k, v, pos)
     ws = nacl.workspace(prob)
     F = nacl.score(prob, q, k, ws)
@@ -115,12 +116,13 @@ def test_score_strided_inputs():
     check_scores(F.cpu().numpy(), Fr, "strided")
 
 
-@pytest.mark.parametrize("P", [40, 160, 700])
+@pytest.mark.parametrize("P", [3, 40, 160, 700])
 def test_score_with_caller_lse(P):
     """With the caller's log-sum-exp (Appendix A.7, Algorithm 2) only the
-    column reduction runs and gives the same scores (P = 160: the proxy-split
-    kernel, a full and a partial proxy group; P = 700: the wide kernel, a full
-    and a partial group of 512)."""
+    column reduction runs and gives the same scores (P = 3: a few-row problem,
+    which with a caller LSE takes the per-wave-tile kernel's single pass;
+    P = 160: the proxy-split kernel, a full and a partial proxy group; P = 700:
+    the wide kernel, a full and a partial group of 512)."""
     w = custom("lse", 1, 3, 1500, 128, P, dtype="bf16", data_seed=3)
     q, k, v = make_layer(w, 0, device="cuda")
     pos = w.proxy_pos

@@ -1,10 +1,11 @@
 """nacl_evict_noalloc (the entry point for callers that cannot allocate)
-against nacl_evict with a caller workspace: two calls in a row on the same
-GPU, the second on a smaller problem (the built-in scratch keeps the first
-call's contents), each compared bit for bit with nacl_evict on the same
-inputs (the same kernels run, so scores, keep sets and compacted rows are
-identical), plus one head against the oracle; health words zero.  A problem
-whose workspace exceeds the built-in scratch is refused."""
+against nacl_evict with a caller workspace: calls in a row on the same
+GPU, the second on a smaller problem and the third on a few-row one (the
+built-in scratch keeps the previous call's contents), each compared bit for
+bit with nacl_evict on the same inputs (the same kernels run, so scores, keep
+sets and compacted rows are identical), plus one head against the oracle;
+health words zero.  A problem whose workspace exceeds the built-in scratch
+is refused."""
 
 import numpy as np
 import pytest
@@ -52,6 +53,8 @@ def _case(w):
 def test_noalloc_matches_evict_twice_smaller_second():
     _case(custom("noalloc_big", 2, 8, 9000, 128, 128, dtype="bf16", inject=True, data_seed=71))
     _case(custom("noalloc_small", 1, 3, 2100, 64, 40, dtype="f32", data_seed=72))
+    # a third call: two proxies, the few-row score path (logits in the scratch)
+    _case(custom("noalloc_rows", 2, 4, 3001, 128, 2, dtype="bf16", data_seed=73))
 
 
 def test_noalloc_refuses_oversized_problems():
