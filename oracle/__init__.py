@@ -7,7 +7,7 @@ calls it, and it shares no code with the GPU library.
 
 from .nacl_oracle import (  # noqa: F401
     SAMPLE_SOFTMAX, SAMPLE_PROPORTIONAL, SAMPLE_UNIFORM,
-    proxy_scores, proxy_scores_grouped, protected_set, budget_split, top_k_lower_index,
+    proxy_scores, proxy_scores_grouped, causal_attention, protected_set, budget_split, top_k_lower_index,
     gumbel_keys, select_head, select, compact, slot_layout, evict,
 )
 from .philox import philox4x32_10, token_words, open_unit, seed_to_key  # noqa: F401

@@ -108,6 +108,48 @@ def proxy_scores_grouped(Q, K, proxy_pos, sm_scale, q_group):
     return F, lse
 
 
+def causal_attention(Q, K, V, sm_scale, q_group=1, rows=None):
+    """The prefill's causal attention and its per-row log-sum-exp: the
+    forward pass whose log-sum-exp the appendix on FlashAttention-2
+    (Appendix A.7, the paragraph before Algorithm 2) hands to the score so
+    that only the column reduction remains.
+
+    For query head hq (K/V head hq // q_group, the grouping of
+    proxy_scores_grouped) and row i:
+        A[i, j] = s * <Q[i], K[j]>, j <= i (causal)
+        lse[i]  = log sum_{j <= i} exp(A[i, j])
+        O[i]    = sum_{j <= i} exp(A[i, j] - lse[i]) * V[j]
+
+    Q: [B, H * q_group, L, D]; K, V: [B, H, L, D].  rows: optional int array
+    of query rows (all rows when None).  Returns (O [B, H * q_group, n, D],
+    lse [B, H * q_group, n]) in float64, n = number of rows.
+    """
+    Q = np.asarray(Q)
+    K = np.asarray(K)
+    V = np.asarray(V)
+    B, H, L, D = K.shape
+    g = int(q_group) if q_group and q_group > 1 else 1
+    if Q.shape[1] != H * g:
+        raise ValueError("Q must have H * q_group heads")
+    r = np.arange(L, dtype=np.int64) if rows is None else np.asarray(rows, dtype=np.int64)
+    s = np.float64(sm_scale)
+    visible = np.arange(L, dtype=np.int64)[None, :] <= r[:, None]   # [n, L]
+    O = np.zeros((B, H * g, r.shape[0], D), dtype=np.float64)
+    lse = np.zeros((B, H * g, r.shape[0]), dtype=np.float64)
+    for b in range(B):
+        for hq in range(H * g):
+            h = hq // g
+            Kh = K[b, h].astype(np.float64)
+            Vh = V[b, h].astype(np.float64)
+            A = s * (Q[b, hq, r, :].astype(np.float64) @ Kh.T)    # [n, L]
+            A = np.where(visible, A, -np.inf)
+            m = A.max(axis=1, keepdims=True)
+            row_lse = m + np.log(np.exp(A - m).sum(axis=1, keepdims=True))
+            O[b, hq] = np.exp(A - row_lse) @ Vh
+            lse[b, hq] = row_lse[:, 0]
+    return O, lse
+
+
 def protected_set(proxy_pos, n_protect):
     """Pi: the proxy tokens kept by default (Section 5.1: proxies are retained).
 
