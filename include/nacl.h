@@ -225,6 +225,26 @@ int nacl_evict_noalloc(const nacl_problem* p, const void* q, const void* k, cons
                        float* scores, int32_t* keep_idx, void* k_out, void* v_out,
                        uint32_t* health, void* stream);
 
+/* Causal attention of the prefill with the log-sum-exp of every query row:
+ * the FlashAttention-2 forward pass whose log-sum-exp Appendix A.7 reuses,
+ * so that the score of a layer runs as the single column reduction of
+ * Algorithm 2 (nacl_score with lse = lse_proxy reads K once).  bf16 only
+ * (NACL_ERR_UNSUPPORTED otherwise); D = 64 or 128; grouped query heads as in
+ * the problem struct: query head hq reads K/V head hq / q_group.
+ * q: device [B, H*q_group, L, D] with q_stride; k, v: device [B,H,L,D] with
+ * k_stride, v_stride; every row stride at least D.
+ * out: device bf16 [B, H*q_group, L, D] contiguous, row i of a query head =
+ * sum over j <= i of softmax_j(sm_scale <q_i, k_j>) v_j (fp32 accumulation,
+ * the probabilities rounded to bf16 for the value product, the row rounded
+ * to bf16 once).
+ * lse: device fp32 [B, H*q_group, L], the natural log of
+ * sum over j <= i of exp(sm_scale <q_i, k_j>).
+ * lse_proxy: optional device fp32 [B, H*q_group, P] receiving lse at the
+ * proxy rows, the layout of nacl_score's lse argument; it needs
+ * p->proxy_pos_dev.  out, lse and lse_proxy overlap nothing else. */
+int nacl_attention(const nacl_problem* p, const void* q, const void* k, const void* v, void* out,
+                   float* lse, float* lse_proxy, void* stream);
+
 /* Static text for a status code. */
 const char* nacl_status_string(int status);
 

@@ -5,5 +5,5 @@ with a thin ctypes binding."""
 from .nacl import (  # noqa: F401
     NaclError, Problem, SAMPLE_PROPORTIONAL, SAMPLE_SOFTMAX, SAMPLE_UNIFORM, EXPORTED,
     LIB_PATH, load_library, workspace_bytes, workspace, score, select, compact, compact_slots, evict,
-    evict_slots,
+    evict_slots, attention,
 )

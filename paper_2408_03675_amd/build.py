@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libnacl.so")
 ARCH = "gfx950"
 
-SOURCES = ["score.hip", "select.hip", "compact.hip", "api.cpp", "noalloc.hip"]
+SOURCES = ["score.hip", "select.hip", "compact.hip", "attention.hip", "api.cpp", "noalloc.hip"]
 
 # Packed fp32 arithmetic stays off: the kernels are written for plain fp32
 # VALU ops.

@@ -537,6 +537,67 @@ int nacl_append(const nacl_problem* p, void* k, void* v, int32_t row0, const voi
   return NACL_OK;
 }
 
+int nacl_attention(const nacl_problem* p, const void* q, const void* k, const void* v, void* out, float* lse,
+                   float* lse_proxy, void* stream) {
+  g_detail[0] = 0;
+  int st = check_problem(p);
+  if (st) return st;
+  if (p->dtype != NACL_BF16) return fail(NACL_ERR_UNSUPPORTED, "attention takes bf16 Q, K, V only");
+  if (!q || !k || !v || !out || !lse) return fail(NACL_ERR_INVALID_ARG, "q, k, v, out and lse must be non-NULL");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(NACL_ERR_INVALID_ARG, "q, k, v and out must be 16-byte aligned");
+  if (lse_proxy && !p->proxy_pos_dev)
+    return fail(NACL_ERR_INVALID_ARG, "lse_proxy needs proxy_pos_dev (the proxy rows on the device)");
+  // Each head's rows are addressed through buffer descriptors with 32-bit
+  // byte offsets, up to 127 rows past L.
+  const int64_t rows[3] = {p->q_stride[2], p->k_stride[2], p->v_stride[2]};
+  for (int t = 0; t < 3; ++t) {
+    if (rows[t] < p->D) return fail(NACL_ERR_INVALID_ARG, "attention needs row strides of at least D");
+    if ((int64_t)p->L * rows[t] * 2 >= ((int64_t)1 << 31) || rows[t] * 2 >= ((int64_t)1 << 24))
+      return fail(NACL_ERR_UNSUPPORTED, "one head's rows span 2 GiB or more");
+  }
+  const int g = q_group_of(p);
+  const int64_t Hq = (int64_t)p->H * g;
+  const uintptr_t o0 = (uintptr_t)out, o1 = o0 + (uintptr_t)(p->B * Hq * p->L * p->D * 2);
+  const uintptr_t l0 = (uintptr_t)lse, l1 = l0 + (uintptr_t)(p->B * Hq * p->L * 4);
+  const uintptr_t x0 = (uintptr_t)lse_proxy, x1 = x0 + (lse_proxy ? (uintptr_t)(p->B * Hq * p->P * 4) : 0);
+  nacl_problem pq = *p;  // Q's extent: H * q_group heads
+  pq.H = (int32_t)Hq;
+  uintptr_t q0, q1, k0, k1, v0, v1;
+  extent(q, p->q_stride, &pq, q0, q1);
+  extent(k, p->k_stride, p, k0, k1);
+  extent(v, p->v_stride, p, v0, v1);
+  const uintptr_t ins[3][2] = {{q0, q1}, {k0, k1}, {v0, v1}};
+  for (int t = 0; t < 3; ++t)
+    if (overlaps(o0, o1, ins[t][0], ins[t][1]) || overlaps(l0, l1, ins[t][0], ins[t][1]) ||
+        (lse_proxy && overlaps(x0, x1, ins[t][0], ins[t][1])))
+      return fail(NACL_ERR_INVALID_ARG, "out, lse or lse_proxy overlaps Q, K or V");
+  if (overlaps(o0, o1, l0, l1) || (lse_proxy && (overlaps(x0, x1, o0, o1) || overlaps(x0, x1, l0, l1))))
+    return fail(NACL_ERR_INVALID_ARG, "out, lse and lse_proxy must not overlap");
+  nacl::AttnLaunch a{};
+  a.B = p->B;
+  a.H = p->H;
+  a.G = g;
+  a.L = p->L;
+  a.n_tiles = (p->L + 127) / 128;
+  a.c2 = p->sm_scale * 1.4426950408889634f;
+  for (int i = 0; i < 3; ++i) {
+    a.qs[i] = p->q_stride[i];
+    a.ks[i] = p->k_stride[i];
+    a.vs[i] = p->v_stride[i];
+  }
+  a.q = static_cast<const __bf16*>(q);
+  a.k = static_cast<const __bf16*>(k);
+  a.v = static_cast<const __bf16*>(v);
+  a.out = static_cast<__bf16*>(out);
+  a.lse = lse;
+  if ((int64_t)a.B * Hq * a.n_tiles >= ((int64_t)1 << 31))
+    return fail(NACL_ERR_UNSUPPORTED, "too many query tiles");
+  hipError_t e = nacl::launch_attention(a, p->D, p->proxy_pos_dev, p->P, lse_proxy, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "attention kernel");
+  return NACL_OK;
+}
+
 int nacl_evict(const nacl_problem* p, const void* q, const void* k, const void* v, int32_t C,
                int32_t Cr, int32_t sampling, uint64_t seed, uint32_t layer, float* scores,
                int32_t* keep_idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,

@@ -189,4 +189,20 @@ struct AppendLaunch {
 
 hipError_t launch_append(const AppendLaunch& L, hipStream_t stream);
 
+// Causal attention of the prefill with each row's log-sum-exp (attention.hip).
+struct AttnLaunch {
+  int B, H, G, L;      // batch, K/V heads, query heads per K/V head, rows
+  int n_tiles;         // 128-row query tiles per head
+  float c2;            // logit scale times log2(e)
+  int64_t qs[3], ks[3], vs[3];  // element strides (q: per query head)
+  const __bf16* q;
+  const __bf16* k;
+  const __bf16* v;
+  __bf16* out;         // [B, H*G, L, D]
+  float* lse;          // [B, H*G, L]
+};
+// Also writes lse_proxy[b, hq, p] = lse[b, hq, pos[p]] when lse_proxy is set.
+hipError_t launch_attention(const AttnLaunch& a, int D, const int32_t* pos, int P, float* lse_proxy,
+                            hipStream_t stream);
+
 }  // namespace nacl

@@ -28,7 +28,8 @@ SAMPLE_PROPORTIONAL = 1
 SAMPLE_UNIFORM = 2
 
 EXPORTED = ("nacl_workspace_bytes", "nacl_score", "nacl_select", "nacl_compact", "nacl_compact_slots",
-            "nacl_append", "nacl_evict", "nacl_evict_slots", "nacl_evict_noalloc", "nacl_status_string",
+            "nacl_append", "nacl_evict", "nacl_evict_slots", "nacl_evict_noalloc", "nacl_attention",
+            "nacl_status_string",
             "nacl_last_error_detail", "nacl_version")
 
 
@@ -83,6 +84,8 @@ def load_library(path=LIB_PATH):
     lib.nacl_evict.restype = ctypes.c_int
     lib.nacl_evict_noalloc.argtypes = [P, vp, vp, vp, i32, i32, i32, u64, u32, vp, vp, vp, vp, vp, vp]
     lib.nacl_evict_noalloc.restype = ctypes.c_int
+    lib.nacl_attention.argtypes = [P, vp, vp, vp, vp, vp, vp, vp]
+    lib.nacl_attention.restype = ctypes.c_int
     lib.nacl_status_string.argtypes = [ctypes.c_int]
     lib.nacl_status_string.restype = ctypes.c_char_p
     lib.nacl_last_error_detail.argtypes = []
@@ -278,6 +281,34 @@ def compact(prob, k, v, keep_idx, k_out=None, v_out=None, in_place=False):
     _check(lib.nacl_compact(prob.ref(), _ptr(k), _ptr(v), _ptr(keep_idx), int(C), _ptr(k_out),
                             _ptr(v_out), _stream(k.device)))
     return k_out, v_out
+
+
+def attention(prob, q, k, v, out=None, lse=None, lse_proxy=False):
+    """Causal attention of the prefill and each row's log-sum-exp (the
+    forward pass whose log-sum-exp Appendix A.7 hands to the score).
+    Returns (out [B, H*q_group, L, D] bf16, lse [B, H*q_group, L] fp32,
+    lse_proxy [B, H*q_group, P] fp32 or None).  lse_proxy=True needs the
+    problem's proxy_pos_dev; the result is nacl_score's lse argument."""
+    lib = load_library()
+    dev = _gpu(k, "k", k.device).device
+    prob.qkv(q, "q", dev, "q")
+    prob.qkv(k, "k", dev, "k")
+    prob.qkv(v, "v", dev, "v")
+    Hq = prob.H * prob.q_group
+    if out is None:
+        out = torch.empty((prob.B, Hq, prob.L, prob.D), dtype=prob.torch_dtype, device=dev)
+    _gpu(out, "out", dev, (prob.B, Hq, prob.L, prob.D), prob.torch_dtype, contiguous=True)
+    if lse is None:
+        lse = torch.empty((prob.B, Hq, prob.L), dtype=torch.float32, device=dev)
+    _gpu(lse, "lse", dev, (prob.B, Hq, prob.L), torch.float32, contiguous=True)
+    lp = None
+    if lse_proxy is True:
+        lp = torch.empty((prob.B, Hq, prob.c.P), dtype=torch.float32, device=dev)
+    elif lse_proxy is not False and lse_proxy is not None:
+        lp = _gpu(lse_proxy, "lse_proxy", dev, (prob.B, Hq, prob.c.P), torch.float32, contiguous=True)
+    _check(lib.nacl_attention(prob.ref(), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(lp),
+                              _stream(k.device)))
+    return out, lse, lp
 
 
 def compact_slots(prob, k, v, keep_idx, slot_idx=None):
