@@ -217,32 +217,39 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
         const int qi = qw0 + 16 * qt + r;
-        float x[4][4];
+        if (masked) {
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (key0 + 16 * kt + 4 * g + i > qi) s[kt][qt][i] = -INFINITY;
+        }
+        // The scale is positive, so the largest logit is the scaled largest
+        // raw product; each exponent is then one FMA.
         float mx = -INFINITY;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float v = s[kt][qt][i] * c2;
-            if (masked && key0 + 16 * kt + 4 * g + i > qi) v = -INFINITY;
-            x[kt][i] = v;
-            mx = fmaxf(mx, v);
-          }
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kt][qt][i]);
         mx = group_max(mx);
-        const float mn = fmaxf(m[qt], mx);
+        const float mn = fmaxf(m[qt], mx * c2);
         const float alpha = __builtin_amdgcn_exp2f(m[qt] - mn);
         m[qt] = mn;
+        float x[4][4];
         float sum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            x[kt][i] = __builtin_amdgcn_exp2f(x[kt][i] - mn);
+            x[kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][qt][i], c2, -mn));
             sum += x[kt][i];
           }
         l[qt] = l[qt] * alpha + sum;
+        // Rescale only when some row of the wave raised its maximum.
+        if (__ballot(alpha != 1.f)) {
 #pragma unroll
-        for (int dt = 0; dt < kDt; ++dt) acc[qt][dt] *= alpha;
+          for (int dt = 0; dt < kDt; ++dt) acc[qt][dt] *= alpha;
+        }
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
           pf[qt][kb2] = bf16x8{(__bf16)x[2 * kb2][0], (__bf16)x[2 * kb2][1], (__bf16)x[2 * kb2][2],
