@@ -21,7 +21,8 @@
 // the other half of a double buffer in LDS after the tile in hand is done,
 // so one barrier per tile separates the stages: K rows with their 16-byte
 // chunks XOR-swizzled (the 16 rows of a fragment read hit distinct banks),
-// V transposed (V^T[d][key], 8-byte chunks of 4 keys XOR-swizzled by d).
+// V transposed (V^T[d][key], each lane's 8 keys of a fragment in one
+// XOR-swizzled 16-byte chunk).
 // (Buffer->LDS loads for K would save the registers, but the compiler makes
 // every LDS read wait for all of them in flight, the next tile's included.)
 // Work-groups are dealt to the 8 XCDs in turn; each XCD takes a contiguous
@@ -151,12 +152,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
             vr, (uint32_t)(j * kAttnKeys + 2 * kp + e) * vrow + (uint32_t)c * 16u, 0, 0);
     }
   };
-  // V^T row d holds 16 chunks of 4 keys; chunk kc sits at position kc ^ (d & 15).
+  // V^T row d (128 bytes) holds the tile's 64 keys permuted so that the 8
+  // keys lane group g contributes to contraction block kb2 (keys 32 kb2 +
+  // 4 g .. + 3 and 32 kb2 + 16 + 4 g .. + 3) form 16-byte chunk 4 kb2 + g,
+  // stored at chunk position (4 kb2 + g) ^ ((d >> 1) & 7): the 16 rows one
+  // fragment read touches then cover every bank once per row parity.
   auto write_vt = [&](int buf) {
+    // keys 2 kp, 2 kp + 1: block kp >> 4, half (kp >> 3) & 1, group (kp >> 1) & 3,
+    // first of the pair at 2 (kp & 1) within its 4 keys
+    const int c16 = 4 * (kp >> 4) + ((kp >> 1) & 3);
+    const int dw = 2 * ((kp >> 3) & 1) + (kp & 1);  // dword within the chunk
 #pragma unroll
     for (int u = 0; u < kVUnits; ++u) {
       const int c = (tid >> 5) + 8 * u;
-      const int kc = kp >> 1;
 #pragma unroll
       for (int jj = 0; jj < 8; ++jj) {
         const int d = 8 * c + jj;
@@ -164,7 +172,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
         // bf16 jj of each row: low or high half of word jj / 2
         const uint32_t lo = (jj & 1) ? (w0 >> 16) : (w0 & 0xFFFFu);
         const uint32_t hi = (jj & 1) ? (w1 & 0xFFFF0000u) : (w1 << 16);
-        *reinterpret_cast<uint32_t*>(vbuf[buf] + d * 128 + ((kc ^ (d & 15)) * 8) + (kp & 1) * 4) = lo | hi;
+        *reinterpret_cast<uint32_t*>(vbuf[buf] + d * 128 + ((c16 ^ ((d >> 1) & 7)) * 16) + dw * 4) = lo | hi;
       }
     }
   };
@@ -212,6 +220,15 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
           s[kt][qt] = t;
         }
       }
+      // Value fragment (A operand of O^T): V^T row d = 16 dt + r, chunk 4 kb2 + g.
+      auto vfrag = [&](int dt, int kb2) {
+        const int d = 16 * dt + r;
+        return __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(vt_base + d * 128 + (((4 * kb2 + g) ^ ((d >> 1) & 7)) * 16)));
+      };
+      // The first d tile's value fragments are read before the exponentials.
+      bf16x8 vcur[2] = {vfrag(0, 0), vfrag(0, 1)};
+      __builtin_amdgcn_sched_barrier(0);
       const bool masked = key0 + kAttnKeys - 1 > qw0;
       bf16x8 pf[2][2];  // [qt][kb2]
 #pragma unroll
@@ -256,19 +273,25 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
                                (__bf16)x[2 * kb2][3], (__bf16)x[2 * kb2 + 1][0], (__bf16)x[2 * kb2 + 1][1],
                                (__bf16)x[2 * kb2 + 1][2], (__bf16)x[2 * kb2 + 1][3]};
       }
-      // O^T += V^T P^T: A = V^T rows d = 16 dt + r, keys 32 kb2 + 4 g .. + 3
-      // and 32 kb2 + 16 + 4 g .. + 3 (chunks 8 kb2 + g and 8 kb2 + 4 + g).
+      // O^T += V^T P^T; the reads of d tile dt + 1 are issued before the
+      // products of d tile dt.
 #pragma unroll
       for (int dt = 0; dt < kDt; ++dt) {
-        const int d = 16 * dt + r;
+        bf16x8 vnxt[2];
+        if (dt + 1 < kDt) {
+          vnxt[0] = vfrag(dt + 1, 0);
+          vnxt[1] = vfrag(dt + 1, 1);
+        }
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-          const u32x2 v0 = *reinterpret_cast<const u32x2*>(vt_base + d * 128 + (((8 * kb2 + g) ^ (d & 15)) * 8));
-          const u32x2 v1 = *reinterpret_cast<const u32x2*>(vt_base + d * 128 + (((8 * kb2 + 4 + g) ^ (d & 15)) * 8));
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{v0[0], v0[1], v1[0], v1[1]});
+        for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
           for (int qt = 0; qt < 2; ++qt)
-            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[qt][kb2], acc[qt][dt], 0, 0, 0);
+            acc[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vcur[kb2], pf[qt][kb2], acc[qt][dt], 0, 0, 0);
+        if (dt + 1 < kDt) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // the two reads
+          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // then the four products
+          vcur[0] = vnxt[0];
+          vcur[1] = vnxt[1];
         }
       }
     }
