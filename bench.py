@@ -66,6 +66,10 @@ def parse():
     ap.add_argument("--generation", action="store_true",
                     help="instead of the benchmark, time generation-phase re-eviction at decode shapes "
                          "(append m rows, evict the C + m cache back to C in place)")
+    ap.add_argument("--prefill", action="store_true",
+                    help="instead of the benchmark, time one layer of Appendix A.7's pipeline: the prefill "
+                         "attention with its log-sum-exp, then the eviction fed with it (score in one pass), "
+                         "beside the eviction that computes the log-sum-exp itself")
     ap.add_argument("--configs", action="store_true",
                     help="instead of the benchmark, print one JSON line per parity workload (GPU times, "
                          "score roofline fraction, oracle rate on a bounded sample of heads)")
@@ -90,6 +94,9 @@ def main():
         return
     if args.generation:
         run_generation(args.workload)
+        return
+    if args.prefill:
+        run_prefill(args.workload)
         return
     w = WORKLOADS[args.workload]
     layers = args.layers or w.layers
@@ -366,6 +373,83 @@ def run_probe(which, w, prob, ws, layer0, out0):
             dst.copy_(src)
     torch.cuda.synchronize()
     log(f"[bench] probe {which} done")
+
+
+def run_prefill(name):
+    """Appendix A.7's pipeline for one layer of a workload: nacl_attention
+    (the causal prefill attention, which also returns each row's
+    log-sum-exp and gathers the proxy rows'), then nacl_score with that
+    log-sum-exp (the column reduction of Algorithm 2 alone: K read once),
+    nacl_select and nacl_compact; beside it the eviction as the benchmark runs
+    it (nacl_evict: two passes over K).  Events around three back-to-back
+    calls, median of three such runs; one JSON line."""
+    import statistics
+    import torch
+    from paper_2408_03675_amd import nacl
+    from synth import WORKLOADS, make_layer
+
+    w = WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    nacl.load_library()
+    q, k, v = make_layer(w, 0, device=dev)
+    pos_dev = torch.tensor(w.proxy_pos, dtype=torch.int32, device=dev)
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, n_protect=w.n_protect, sm_scale=w.scale,
+                                     proxy_pos_dev=pos_dev)
+    ws = nacl.workspace(prob, dev)
+    Hq = w.H
+    out = torch.empty_like(q)
+    lse = torch.empty((w.B, Hq, w.L), dtype=torch.float32, device=dev)
+    lp = torch.empty((w.B, Hq, w.P), dtype=torch.float32, device=dev)
+    F = torch.empty((w.B, w.H, w.L), dtype=torch.float32, device=dev)
+    keep = torch.empty((w.B, w.H, w.C), dtype=torch.int32, device=dev)
+    ko = torch.empty((w.B, w.H, w.C, w.D), dtype=q.dtype, device=dev)
+    vo = torch.empty_like(ko)
+
+    def attention():
+        nacl.attention(prob, q, k, v, out=out, lse=lse, lse_proxy=lp)
+
+    def score_lse():
+        nacl.score(prob, q, k, ws, lse=lp, out=F)
+
+    def evict_lse():
+        nacl.score(prob, q, k, ws, lse=lp, out=F)
+        nacl.select(prob, F, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, 0, ws=ws, out=keep)
+        nacl.compact(prob, k, v, keep, k_out=ko, v_out=vo)
+
+    def score_two_pass():
+        nacl.score(prob, q, k, ws, out=F)
+
+    def evict_two_pass():
+        nacl.evict(prob, q, k, v, w.C, w.Cr, nacl.SAMPLE_SOFTMAX, w.rng_seed, 0, ws=ws, scores=F,
+                   keep_idx=keep, k_out=ko, v_out=vo)
+
+    def med(fn, reps=3, rounds=3):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(rounds):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / reps)
+        return statistics.median(ts)
+
+    t_att = med(attention)
+    log(f"[prefill] attention {t_att:.3f} ms")
+    t_sl, t_el = med(score_lse, 10), med(evict_lse, 10)
+    t_s2, t_e2 = med(score_two_pass, 10), med(evict_two_pass, 10)
+    flops = 4.0 * w.D * (w.L * (w.L + 1) / 2) * w.B * Hq
+    print(json.dumps({
+        "workload": name, "B": w.B, "H": w.H, "L": w.L, "D": w.D, "P": w.P, "C": w.C, "Cr": w.Cr,
+        "attention_ms": round(t_att, 3),
+        "attention_tflops": round(flops / t_att / 1e9, 1),
+        "attention_mfma_frac": round(flops / t_att / 1e9 / 2500.0, 3),
+        "score_with_lse_us": round(t_sl * 1e3, 1), "evict_with_lse_us": round(t_el * 1e3, 1),
+        "score_two_pass_us": round(t_s2 * 1e3, 1), "evict_two_pass_us": round(t_e2 * 1e3, 1),
+    }), flush=True)
 
 
 def run_configs(oracle_seconds=5.0):

@@ -157,22 +157,34 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
   // 4 g .. + 3 and 32 kb2 + 16 + 4 g .. + 3) form 16-byte chunk 4 kb2 + g,
   // stored at chunk position (4 kb2 + g) ^ ((d >> 1) & 7): the 16 rows one
   // fragment read touches then cover every bank once per row parity.
-  auto write_vt = [&](int buf) {
+  // Per V unit: the byte offset of d = 8 c + 2 h (h = 0..3) in its V^T row
+  // pair, chunk swizzle included; d = 8 c + 2 h + 1 is the next row.
+  uint32_t vto[kVUnits][4];
+  {
     // keys 2 kp, 2 kp + 1: block kp >> 4, half (kp >> 3) & 1, group (kp >> 1) & 3,
-    // first of the pair at 2 (kp & 1) within its 4 keys
+    // the first of them at 2 (kp & 1) within its 4 keys
     const int c16 = 4 * (kp >> 4) + ((kp >> 1) & 3);
     const int dw = 2 * ((kp >> 3) & 1) + (kp & 1);  // dword within the chunk
 #pragma unroll
     for (int u = 0; u < kVUnits; ++u) {
       const int c = (tid >> 5) + 8 * u;
 #pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const int d = 8 * c + 2 * h;
+        vto[u][h] = (uint32_t)(d * 128 + ((c16 ^ ((d >> 1) & 7)) * 16) + dw * 4);
+      }
+    }
+  }
+  auto write_vt = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < kVUnits; ++u) {
+#pragma unroll
       for (int jj = 0; jj < 8; ++jj) {
-        const int d = 8 * c + jj;
-        const uint32_t w0 = vreg[u][0][jj >> 1], w1 = vreg[u][1][jj >> 1];
-        // bf16 jj of each row: low or high half of word jj / 2
-        const uint32_t lo = (jj & 1) ? (w0 >> 16) : (w0 & 0xFFFFu);
-        const uint32_t hi = (jj & 1) ? (w1 & 0xFFFF0000u) : (w1 << 16);
-        *reinterpret_cast<uint32_t*>(vbuf[buf] + d * 128 + ((c16 ^ ((d >> 1) & 7)) * 16) + dw * 4) = lo | hi;
+        // bf16 jj of rows 2 kp (low half) and 2 kp + 1 (high half): bytes
+        // 2 (jj mod 2) .. + 1 of word jj / 2 of each
+        const uint32_t w = __builtin_amdgcn_perm(vreg[u][1][jj >> 1], vreg[u][0][jj >> 1],
+                                                 (jj & 1) ? 0x07060302u : 0x05040100u);
+        *reinterpret_cast<uint32_t*>(vbuf[buf] + vto[u][jj >> 1] + (jj & 1) * 128) = w;
       }
     }
   };
@@ -235,11 +247,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
       for (int qt = 0; qt < 2; ++qt) {
         const int qi = qw0 + 16 * qt + r;
         if (masked) {
+          // key key0 + 16 kt + 4 g + i is past row qi iff 16 kt + i > lim
+          const int lim = qi - key0 - 4 * g;
 #pragma unroll
           for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              if (key0 + 16 * kt + 4 * g + i > qi) s[kt][qt][i] = -INFINITY;
+              if (16 * kt + i > lim) s[kt][qt][i] = -INFINITY;
         }
         // The scale is positive, so the largest logit is the scaled largest
         // raw product; each exponent is then one FMA.
