@@ -194,3 +194,30 @@ def test_q_group_validation(lib):
     p4 = _prob()
     p4.c.q_group = 4
     assert nacl.workspace_bytes(p4) > n1
+
+
+def test_attention_checks(lib):
+    """nacl_attention refuses, before any launch: fp32 inputs, missing
+    pointers, a proxy gather without device positions, row strides below D,
+    and outputs overlapping an input or each other."""
+    k = 1 << 30
+    kbytes = 2 * 4 * 1000 * 128 * 2  # one [2, 4, 1000, 128] bf16 tensor
+    Q, K, V = (ctypes.c_void_p(k + i * kbytes) for i in (0, 1, 2))
+    OUT = ctypes.c_void_p(k + 3 * kbytes)
+    LSE = ctypes.c_void_p(k + 4 * kbytes)
+    LP = ctypes.c_void_p(k + 5 * kbytes)
+    p32 = _prob(dtype="f32")
+    assert lib.nacl_attention(p32.ref(), Q, K, V, OUT, LSE, None, None) == nacl.NACL_ERR_UNSUPPORTED
+    p = _prob()
+    assert lib.nacl_attention(p.ref(), Q, K, V, None, LSE, None, None) == nacl.NACL_ERR_INVALID_ARG
+    assert lib.nacl_attention(p.ref(), Q, K, V, OUT, None, None, None) == nacl.NACL_ERR_INVALID_ARG
+    # lse_proxy without proxy_pos_dev
+    assert lib.nacl_attention(p.ref(), Q, K, V, OUT, LSE, LP, None) == nacl.NACL_ERR_INVALID_ARG
+    # output inside K, log-sum-exp inside the output
+    assert lib.nacl_attention(p.ref(), Q, K, V, ctypes.c_void_p(k + kbytes + 256), LSE, None,
+                              None) == nacl.NACL_ERR_INVALID_ARG
+    assert lib.nacl_attention(p.ref(), Q, K, V, OUT, ctypes.c_void_p(k + 3 * kbytes + 512), None,
+                              None) == nacl.NACL_ERR_INVALID_ARG
+    # K rows overlapping (row stride 0)
+    ps = nacl.Problem(2, 4, 1000, 128, "bf16", list(range(900, 1000)), k_stride=(4 * 1000 * 128, 1000 * 128, 0))
+    assert lib.nacl_attention(ps.ref(), Q, K, V, OUT, LSE, None, None) == nacl.NACL_ERR_INVALID_ARG
