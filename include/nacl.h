@@ -241,7 +241,9 @@ int nacl_evict_noalloc(const nacl_problem* p, const void* q, const void* k, cons
  * sum over j <= i of exp(sm_scale <q_i, k_j>).
  * lse_proxy: optional device fp32 [B, H*q_group, P] receiving lse at the
  * proxy rows, the layout of nacl_score's lse argument; it needs
- * p->proxy_pos_dev.  out, lse and lse_proxy overlap nothing else. */
+ * p->proxy_pos_dev.  out, lse and lse_proxy overlap nothing else.  The
+ * problem is validated as for every call (its proxy fields included), but
+ * the proxies change nothing except which rows lse_proxy receives. */
 int nacl_attention(const nacl_problem* p, const void* q, const void* k, const void* v, void* out,
                    float* lse, float* lse_proxy, void* stream);
 

@@ -340,13 +340,16 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_fwd_kernel(AttnLaunch a)
   }
 }
 
-// lse_proxy[b, hq, p] = lse[b, hq, pos[p]].
+// lse_proxy[b, hq, p] = lse[b, hq, pos[p]] (NaN for a position outside
+// [0, L), which a device copy that disagrees with the validated host
+// positions could hold; nothing outside the head is read).
 __global__ __launch_bounds__(256) void lse_gather_kernel(const float* lse, const int32_t* pos, int L, int P,
                                                          int64_t n, float* out) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const int64_t bh = i / P;
-  out[i] = lse[bh * L + pos[i - bh * P]];
+  const int j = pos[i - bh * P];
+  out[i] = j >= 0 && j < L ? lse[bh * L + j] : __builtin_nanf("");
 }
 
 }  // namespace
