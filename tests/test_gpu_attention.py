@@ -9,7 +9,6 @@ is held to 1e-4 absolute.  The output rounds each probability to bf16
 to bf16 once more, so |O - O_ref| <= 2^-9 max|V| + 2^-9 |O_ref| <= 2^-8 max|V|;
 the test allows 4.5e-3 max|V|."""
 
-import math
 import sys
 
 import numpy as np
@@ -129,6 +128,21 @@ def test_attention_prefill_32k_sampled_rows():
         sl = slice(h, h + 1)
         _check(out[b:b + 1, sl], lse[b:b + 1, sl], q[b:b + 1, sl], k[b:b + 1, sl], v[b:b + 1, sl],
                prob.c.sm_scale, 1, f"32k b{b} h{h}", rows=rows)
+
+
+def test_attention_d64_grouped_4k_sampled_rows():
+    """Head dim 64 with two query heads per K/V head over 4097 tokens (33
+    query tiles of 128 rows per head, the last holding one row): sampled rows
+    of every head, and every log-sum-exp finite."""
+    B, H, g, L, D, P = 2, 4, 2, 4097, 64, 64
+    w = custom("gqa_d64_4k", B, H, L, D, P, dtype="bf16", data_seed=41)
+    q, k, v = make_grouped_layer(w, g, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos)
+    out, lse, _ = nacl.attention(prob, q, k, v)
+    torch.cuda.synchronize()
+    assert torch.isfinite(lse).all()
+    rows = np.array([0, 63, 64, 127, 128, 255, 256, 2048, 4095, 4096])
+    _check(out, lse, q, k, v, prob.c.sm_scale, g, "gqa_d64_4k", rows=rows)
 
 
 def test_attention_rejects_unsupported():
