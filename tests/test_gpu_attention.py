@@ -145,6 +145,19 @@ def test_attention_d64_grouped_4k_sampled_rows():
     _check(out, lse, q, k, v, prob.c.sm_scale, g, "gqa_d64_4k", rows=rows)
 
 
+@pytest.mark.parametrize("L,g,scale", [(128, 1, 0.05), (256, 8, None), (2, 1, 2.0)])
+def test_attention_tile_multiples_and_scales(L, g, scale):
+    """Exact multiples of the 128-row and 64-key tiles, eight query heads per
+    K/V head, two rows, and logit scales other than 1/sqrt(D)."""
+    B, H, D = 1, 2, 128
+    w = custom(f"edge_{L}_{g}", B, H, L, D, 1, dtype="bf16", data_seed=L + g)
+    q, k, v = make_grouped_layer(w, g, device="cuda") if g > 1 else make_layer(w, device="cuda")
+    prob = nacl.Problem.from_tensors(q, k, v, w.proxy_pos, sm_scale=scale)
+    out, lse, _ = nacl.attention(prob, q, k, v)
+    torch.cuda.synchronize()
+    _check(out, lse, q, k, v, prob.c.sm_scale, g, f"edge L{L} g{g}")
+
+
 def test_attention_rejects_unsupported():
     q = torch.zeros((1, 1, 16, 64), dtype=torch.float32, device="cuda")
     prob = nacl.Problem.from_tensors(q, q, q, [3])
